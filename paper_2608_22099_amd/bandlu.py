@@ -1,0 +1,266 @@
+"""Thin Python binding of libbandlu.so (the C ABI in include/bandlu.h).
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels.  Tensors must be float64 (int32 for pivots) CUDA/ROCm tensors,
+C-contiguous in their last dimension, on the current device; work is enqueued
+on torch's current stream.  If the library is missing this module raises on
+import -- there is no fallback.
+
+Storage convention: a torch tensor ``T`` of shape (n, ld) holds the
+column-major matrix A with ``T[j, i] = A[i, j]`` (row j of T is column j of A,
+ld >= n is the leading dimension).  Band arrays use the same convention with
+shape (n, ldab); batched arrays add a leading batch dimension.
+
+Names follow the paper's path (Sec. II-A, Listing 2): band_detect (identify),
+dense_to_band (convert), band_getrf / band_getrf_batched (specialised LU),
+band_getrs / band_getrs_batched (solve), and the host policy
+speedup_predicate / structure_aware_lu (Sec. II-B speedup constraint).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libbandlu.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(
+        f"{LIB_PATH} is missing: build it with `python -m paper_2608_22099_amd.build` "
+        "(there is no fallback implementation)")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+_i64 = ctypes.c_int64
+_vp = ctypes.c_void_p
+
+EXPORTS = {
+    "band_detect": [_vp, _i64, _i64, _i64, _i64, _vp, _vp],
+    "band_detect_batched": [_vp, _i64, _i64, _i64, _i64, _i64, _i64, _vp, _vp, _vp],
+    "dense_to_band": [_vp, _i64, _i64, _i64, _i64, _vp, _i64, _vp],
+    "dense_to_band_batched": [_vp, _i64, _i64, _i64, _i64, _i64, _vp, _i64, _i64, _i64, _vp],
+    "band_getrf": [_i64, _i64, _i64, _vp, _i64, _vp, _vp, _vp],
+    "band_getrf_batched": [_i64, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _vp, _i64, _vp],
+    "band_getrs": [_i64, _i64, _i64, _i64, _vp, _i64, _vp, _vp, _i64, _vp],
+    "band_getrs_batched": [_i64, _i64, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _vp, _i64, _i64,
+                           _i64, _vp],
+    "band_getrf_variant": [_i64, _i64, _i64, _i64],
+    "band_status_string": [ctypes.c_int],
+    "band_last_error": [],
+}
+for _name, _args in EXPORTS.items():
+    _f = getattr(_lib, _name)
+    _f.argtypes = _args
+    _f.restype = ctypes.c_char_p if _name in ("band_status_string", "band_last_error") \
+        else ctypes.c_int
+
+VARIANTS = {1: "window", 2: "window_g16", 3: "generic", 4: "blocked"}
+
+
+class BandLUError(RuntimeError):
+    def __init__(self, fn, status):
+        self.status = status
+        msg = _lib.band_last_error().decode() or _lib.band_status_string(status).decode()
+        super().__init__(f"{fn} failed with status {status}: {msg}")
+
+
+def _call(name, *args):
+    rc = getattr(_lib, name)(*args)
+    if rc != 0:
+        raise BandLUError(name, rc)
+    return rc
+
+
+def _stream():
+    return _vp(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    return _vp(t.data_ptr()) if t is not None and t.numel() else _vp(0)
+
+
+def _check(t, dtype, name, ndim=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch.Tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name}: must be a GPU tensor")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name}: expected {ndim} dims, got {t.dim()}")
+    if t.numel() and t.stride(-1) != 1:
+        raise ValueError(f"{name}: last dimension must be contiguous")
+
+
+def _ld(t):
+    """Leading dimension of a (.., n, ld) tensor whose rows are the columns of A."""
+    return max(1, t.stride(-2)) if t.dim() >= 2 and t.shape[-2] > 1 else max(1, t.shape[-1])
+
+
+# ------------------------------------------------------------------ detect --
+def band_detect(A, kl_cap=-1, ku_cap=-1, out=None):
+    """(kl, ku, exceeded) of A as a device int64 tensor of 3 (no host sync)."""
+    _check(A, torch.float64, "A", 2)
+    n = A.shape[0]
+    if out is None:
+        out = torch.empty(3, dtype=torch.int64, device=A.device)
+    _call("band_detect", _ptr(A), n, max(_ld(A), n, 1), kl_cap, ku_cap, _ptr(out), _stream())
+    return out
+
+
+def band_detect_batched(A, kl_cap=-1, ku_cap=-1, out=None, dmax=None):
+    """Per-matrix (batch, 3) and batch-max (3,) device int64 tensors."""
+    _check(A, torch.float64, "A", 3)
+    batch, n = A.shape[0], A.shape[1]
+    if out is None:
+        out = torch.empty((batch, 3), dtype=torch.int64, device=A.device)
+    if dmax is None:
+        dmax = torch.empty(3, dtype=torch.int64, device=A.device)
+    stride = A.stride(0) if batch > 1 else max(_ld(A), n, 1) * n
+    _call("band_detect_batched", _ptr(A), n, max(_ld(A), n, 1), stride, batch, kl_cap, ku_cap,
+          _ptr(out), _ptr(dmax), _stream())
+    return out, dmax
+
+
+# ----------------------------------------------------------------- convert --
+def dense_to_band(A, kl, ku, AB=None, ldab=None):
+    """Pack A into an (n, ldab) band tensor in xGBTRF layout."""
+    _check(A, torch.float64, "A", 2)
+    n = A.shape[0]
+    if AB is None:
+        ldab = ldab or 2 * kl + ku + 1
+        AB = torch.empty((n, ldab), dtype=torch.float64, device=A.device)
+    _check(AB, torch.float64, "AB", 2)
+    _call("dense_to_band", _ptr(A), n, max(_ld(A), n, 1), kl, ku, _ptr(AB), max(_ld(AB), 1),
+          _stream())
+    return AB
+
+
+def dense_to_band_batched(A, kl, ku, AB=None, ldab=None):
+    _check(A, torch.float64, "A", 3)
+    batch, n = A.shape[0], A.shape[1]
+    if AB is None:
+        ldab = ldab or 2 * kl + ku + 1
+        AB = torch.empty((batch, n, ldab), dtype=torch.float64, device=A.device)
+    _check(AB, torch.float64, "AB", 3)
+    lda, ldab_ = max(_ld(A), n, 1), max(_ld(AB), 1)
+    sA = A.stride(0) if batch > 1 else lda * n
+    sAB = AB.stride(0) if batch > 1 else ldab_ * n
+    _call("dense_to_band_batched", _ptr(A), n, lda, sA, kl, ku, _ptr(AB), ldab_, sAB, batch,
+          _stream())
+    return AB
+
+
+# ------------------------------------------------------------------- getrf --
+def band_getrf(AB, kl, ku, ipiv=None, info=None):
+    """In-place band LU; returns (ipiv int32 (n,), info int32 (1,)) on device."""
+    _check(AB, torch.float64, "AB", 2)
+    n = AB.shape[0]
+    if ipiv is None:
+        ipiv = torch.empty(n, dtype=torch.int32, device=AB.device)
+    if info is None:
+        info = torch.empty(1, dtype=torch.int32, device=AB.device)
+    _call("band_getrf", n, kl, ku, _ptr(AB), max(_ld(AB), 1), _ptr(ipiv), _ptr(info), _stream())
+    return ipiv, info
+
+
+def band_getrf_batched(AB, kl, ku, ipiv=None, info=None):
+    """In-place batched band LU; returns (ipiv (batch, n), info (batch,))."""
+    _check(AB, torch.float64, "AB", 3)
+    batch, n = AB.shape[0], AB.shape[1]
+    if ipiv is None:
+        ipiv = torch.empty((batch, n), dtype=torch.int32, device=AB.device)
+    if info is None:
+        info = torch.empty(batch, dtype=torch.int32, device=AB.device)
+    ldab = max(_ld(AB), 1)
+    sAB = AB.stride(0) if batch > 1 else ldab * n
+    sP = ipiv.stride(0) if batch > 1 else n
+    _call("band_getrf_batched", n, kl, ku, _ptr(AB), ldab, sAB, _ptr(ipiv), sP, _ptr(info), batch,
+          _stream())
+    return ipiv, info
+
+
+def band_getrf_variant(n, kl, ku, batch=1):
+    v = _lib.band_getrf_variant(n, kl, ku, batch)
+    if v < 0:
+        raise BandLUError("band_getrf_variant", v)
+    return VARIANTS[v]
+
+
+# ------------------------------------------------------------------- getrs --
+def band_getrs(AB, kl, ku, ipiv, B):
+    """Solve in place; B has shape (nrhs, ldb) with B[k, i] = row i of rhs k."""
+    _check(AB, torch.float64, "AB", 2)
+    _check(ipiv, torch.int32, "ipiv", 1)
+    _check(B, torch.float64, "B", 2)
+    n = AB.shape[0]
+    nrhs = B.shape[0]
+    ldb = max(_ld(B), n, 1)
+    _call("band_getrs", n, kl, ku, nrhs, _ptr(AB), max(_ld(AB), 1), _ptr(ipiv), _ptr(B), ldb,
+          _stream())
+    return B
+
+
+def band_getrs_batched(AB, kl, ku, ipiv, B):
+    """Batched solve in place; B has shape (batch, nrhs, ldb)."""
+    _check(AB, torch.float64, "AB", 3)
+    _check(ipiv, torch.int32, "ipiv", 2)
+    _check(B, torch.float64, "B", 3)
+    batch, n = AB.shape[0], AB.shape[1]
+    nrhs = B.shape[1]
+    ldab = max(_ld(AB), 1)
+    ldb = max(_ld(B), n, 1)
+    sAB = AB.stride(0) if batch > 1 else ldab * n
+    sP = ipiv.stride(0) if batch > 1 else n
+    sB = B.stride(0) if batch > 1 else ldb * nrhs
+    _call("band_getrs_batched", n, kl, ku, nrhs, _ptr(AB), ldab, sAB, _ptr(ipiv), sP, _ptr(B),
+          ldb, sB, batch, _stream())
+    return B
+
+
+# ------------------------------------------------------------- host policy --
+def op_counts(n, kl, ku):
+    """Operation counts of Sec. II-A for one n x n matrix with bandwidths (kl, ku):
+    identify I = n^2 reads, convert C = (2kl+ku+1) n band slots, specialised
+    f = 2 n kl (kl+ku+1) flops (banded LU including pivot fill), generic
+    F = 2 n^3 / 3 flops (dense LU)."""
+    I = n * n
+    C = (2 * kl + ku + 1) * n
+    f = 2 * n * kl * (kl + ku + 1)
+    F = 2.0 * n ** 3 / 3.0
+    return I, C, f, F
+
+
+def speedup_predicate(n, kl, ku):
+    """Sec. II-B speedup constraint I + C + f < F: take the banded branch."""
+    I, C, f, F = op_counts(n, kl, ku)
+    return I + C + f < F
+
+
+class BandLU:
+    """Result of structure_aware_lu on the banded branch."""
+
+    def __init__(self, AB, kl, ku, ipiv, info):
+        self.AB, self.kl, self.ku, self.ipiv, self.info = AB, kl, ku, ipiv, info
+
+    def solve(self, B):
+        return band_getrs(self.AB, self.kl, self.ku, self.ipiv, B)
+
+
+def structure_aware_lu(A, kl_cap=-1, ku_cap=-1):
+    """Listing 2 on the GPU: detect, and if the speedup constraint holds,
+    convert and factor with the banded LU; otherwise factor densely.
+
+    Returns ("banded", BandLU) or ("dense", (LU, pivots)) where the dense
+    branch is the generic algorithm F (rocSOLVER getrf via torch).
+    """
+    out = band_detect(A, kl_cap, ku_cap)
+    kl, ku, exceeded = (int(v) for v in out.cpu())  # the one device->host copy
+    n = A.shape[0]
+    if not exceeded and speedup_predicate(n, kl, ku):
+        AB = dense_to_band(A, kl, ku)
+        ipiv, info = band_getrf(AB, kl, ku)
+        return "banded", BandLU(AB, kl, ku, ipiv, info)
+    return "dense", torch.linalg.lu_factor(A[:, :n].transpose(0, 1))

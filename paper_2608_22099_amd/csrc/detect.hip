@@ -1,0 +1,215 @@
+// Step 1 of the structure-aware strategy (Sec. II-A, cost I(N); Sec. III-A):
+// find the lower and upper bandwidths of a dense column-major matrix.
+//
+// The scan is HBM-bound: every element is read once (8 bytes per element, one
+// compare each).  Each wavefront owns a contiguous run of columns of the
+// (batched) matrix, so it streams consecutive memory.  Within a column every
+// lane reads 16 bytes per load (two rows) and several loads are in flight per
+// lane; rows visited by one lane increase monotonically, so the first and last
+// nonzero row of the lane's share of a column are kept with one compare and a
+// select each.  Lane maxima of (last - j) and (j - first) are reduced across the
+// wave once per matrix and published with one atomic max per value.
+#include <climits>
+
+#include <algorithm>
+
+#include "common.hpp"
+
+namespace bandlu {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kUnroll = 8;
+typedef double dbl2 __attribute__((ext_vector_type(2)));
+
+struct DetectParams {
+    const double *A;
+    int64_t n, lda, strideA;
+    int64_t total_cols;     // n * batch
+    int64_t cols_per_wave;  // contiguous run of columns per wavefront
+    int64_t kl_cap, ku_cap; // INT64_MAX when not capped
+    unsigned long long *out;   // [3 * batch]
+    unsigned long long *dmax;  // [3] or null
+};
+
+__global__ void detect_init(unsigned long long *out, int64_t count, unsigned long long *dmax) {
+    int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    for (; i < count; i += int64_t(gridDim.x) * blockDim.x) out[i] = 0ull;
+    if (dmax && blockIdx.x == 0 && threadIdx.x < 3) dmax[threadIdx.x] = 0ull;
+}
+
+// Publish the wave's bandwidths of matrix b.
+__device__ inline void detect_flush(const DetectParams &P, int64_t b, int kl_l, int ku_l, int lane) {
+    int kl_w = wave_max_i32(kl_l);
+    int ku_w = wave_max_i32(ku_l);
+    if (lane == 0) {
+        unsigned long long *o = P.out + 3 * b;
+        if (kl_w > 0) atomicMax(o + 0, (unsigned long long)kl_w);
+        if (ku_w > 0) atomicMax(o + 1, (unsigned long long)ku_w);
+        bool ex = (int64_t)kl_w > P.kl_cap || (int64_t)ku_w > P.ku_cap;
+        if (ex) atomicMax(o + 2, 1ull);
+        if (P.dmax) {
+            if (kl_w > 0) atomicMax(P.dmax + 0, (unsigned long long)kl_w);
+            if (ku_w > 0) atomicMax(P.dmax + 1, (unsigned long long)ku_w);
+            if (ex) atomicMax(P.dmax + 2, 1ull);
+        }
+    }
+}
+
+template <bool VEC, bool CAPS>
+__global__ __launch_bounds__(kThreads) void detect_kernel(DetectParams P) {
+    const int lane = threadIdx.x & 63;
+    const int64_t wave = (int64_t(blockIdx.x) * kThreads + threadIdx.x) >> 6;
+    const int64_t g0 = wave * P.cols_per_wave;
+    const int64_t g1 = min(g0 + P.cols_per_wave, P.total_cols);
+    if (g0 >= g1) return;
+    const int64_t n = P.n;
+    int64_t b = g0 / n;
+    int64_t j = g0 - b * n;
+    int kl_l = 0, ku_l = 0;
+    bool skip = false;  // matrix b already known to exceed a cap
+    for (int64_t g = g0; g < g1; ++g) {
+        if (CAPS && !skip) {
+            skip = __hip_atomic_load(P.out + 3 * b + 2, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT) != 0ull;
+        }
+        if (!skip) {
+            const double *col = P.A + b * P.strideA + j * P.lda;
+            int first = INT_MAX, last = -1;
+            if (VEC) {
+                const dbl2 *c2 = reinterpret_cast<const dbl2 *>(col);
+                const int n2 = int(n >> 1);
+                for (int base = 0; base < n2; base += 64 * kUnroll) {
+                    dbl2 v[kUnroll];
+#pragma unroll
+                    for (int u = 0; u < kUnroll; ++u) {
+                        int idx = base + u * 64 + lane;
+                        v[u] = idx < n2 ? __builtin_nontemporal_load(c2 + idx) : dbl2{0.0, 0.0};
+                    }
+#pragma unroll
+                    for (int u = 0; u < kUnroll; ++u) {
+                        int i0 = 2 * (base + u * 64 + lane);
+                        if (v[u].x != 0.0) { last = i0; first = min(first, i0); }
+                        if (v[u].y != 0.0) { last = i0 + 1; first = min(first, i0 + 1); }
+                    }
+                }
+                if ((n & 1) && lane == 0) {
+                    int i0 = int(n - 1);
+                    if (col[i0] != 0.0) { last = i0; first = min(first, i0); }
+                }
+            } else {
+                const int nn = int(n);
+                for (int base = 0; base < nn; base += 64 * kUnroll) {
+                    double v[kUnroll];
+#pragma unroll
+                    for (int u = 0; u < kUnroll; ++u) {
+                        int idx = base + u * 64 + lane;
+                        v[u] = idx < nn ? __builtin_nontemporal_load(col + idx) : 0.0;
+                    }
+#pragma unroll
+                    for (int u = 0; u < kUnroll; ++u) {
+                        int i0 = base + u * 64 + lane;
+                        if (v[u] != 0.0) { last = i0; first = min(first, i0); }
+                    }
+                }
+            }
+            const int jj = int(j);
+            if (last >= 0) {
+                kl_l = max(kl_l, last - jj);
+                ku_l = max(ku_l, jj - first);
+            }
+            if (CAPS) {
+                bool ex = (int64_t)kl_l > P.kl_cap || (int64_t)ku_l > P.ku_cap;
+                // tell every other wave of this matrix to stop early
+                if (__any(ex) && lane == 0)
+                    __hip_atomic_store(P.out + 3 * b + 2, 1ull, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        if (++j == n) {
+            detect_flush(P, b, kl_l, ku_l, lane);
+            kl_l = ku_l = 0;
+            skip = false;
+            j = 0;
+            ++b;
+        }
+    }
+    if (j != 0) detect_flush(P, b, kl_l, ku_l, lane);
+}
+
+int launch_detect(const double *dA, int64_t n, int64_t lda, int64_t strideA, int64_t batch,
+                  int64_t kl_cap, int64_t ku_cap, int64_t *d_out, int64_t *d_max,
+                  hipStream_t s) {
+    const int64_t count = 3 * batch;
+    {
+        int blocks = (int)std::min<int64_t>((count + 255) / 256, 1024);
+        if (blocks < 1) blocks = 1;
+        hipLaunchKernelGGL(detect_init, dim3(blocks), dim3(256), 0, s,
+                           reinterpret_cast<unsigned long long *>(d_out), count,
+                           reinterpret_cast<unsigned long long *>(d_max));
+        BANDLU_CHECK_LAUNCH("band_detect init");
+    }
+    if (n == 0 || batch == 0) return BANDLU_OK;
+    DetectParams P;
+    P.A = dA;
+    P.n = n;
+    P.lda = lda;
+    P.strideA = strideA;
+    P.total_cols = n * batch;
+    const int64_t max_waves = int64_t(device_cu_count()) * 32;  // 8 waves per SIMD
+    const int64_t waves = std::min(P.total_cols, max_waves);
+    P.cols_per_wave = (P.total_cols + waves - 1) / waves;
+    const int64_t used_waves = (P.total_cols + P.cols_per_wave - 1) / P.cols_per_wave;
+    const int64_t blocks = (used_waves + (kThreads / 64) - 1) / (kThreads / 64);
+    P.kl_cap = kl_cap < 0 ? INT64_MAX : kl_cap;
+    P.ku_cap = ku_cap < 0 ? INT64_MAX : ku_cap;
+    P.out = reinterpret_cast<unsigned long long *>(d_out);
+    P.dmax = reinterpret_cast<unsigned long long *>(d_max);
+    const bool caps = kl_cap >= 0 || ku_cap >= 0;
+    const bool vec = (reinterpret_cast<uintptr_t>(dA) % 16 == 0) && (lda % 2 == 0) &&
+                     (batch == 1 || strideA % 2 == 0);
+    auto k = vec ? (caps ? detect_kernel<true, true> : detect_kernel<true, false>)
+                 : (caps ? detect_kernel<false, true> : detect_kernel<false, false>);
+    hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(kThreads), 0, s, P);
+    BANDLU_CHECK_LAUNCH("band_detect");
+    return BANDLU_OK;
+}
+
+}  // namespace
+}  // namespace bandlu
+
+using namespace bandlu;
+
+extern "C" int band_detect(const double *dA, int64_t n, int64_t lda, int64_t kl_cap,
+                           int64_t ku_cap, int64_t *d_out, void *stream) {
+    clear_error();
+    BANDLU_ARG(n >= 0, 2, "band_detect: n = %lld < 0", (long long)n);
+    BANDLU_ARG(lda >= (n > 1 ? n : 1), 3, "band_detect: lda = %lld < max(1, n)", (long long)lda);
+    BANDLU_ARG(d_out != nullptr, 6, "band_detect: d_out is null");
+    BANDLU_ARG(n == 0 || dA != nullptr, 1, "band_detect: dA is null");
+    if (n > kMaxN) {
+        set_error("band_detect: n >= 2^31 is not supported");
+        return BANDLU_ERR_UNSUPPORTED;
+    }
+    return launch_detect(dA, n, lda, lda * n, 1, kl_cap, ku_cap, d_out, nullptr,
+                         as_stream(stream));
+}
+
+extern "C" int band_detect_batched(const double *dA, int64_t n, int64_t lda, int64_t strideA,
+                                   int64_t batch, int64_t kl_cap, int64_t ku_cap,
+                                   int64_t *d_out, int64_t *d_max, void *stream) {
+    clear_error();
+    BANDLU_ARG(n >= 0, 2, "band_detect_batched: n = %lld < 0", (long long)n);
+    BANDLU_ARG(lda >= (n > 1 ? n : 1), 3, "band_detect_batched: lda < max(1, n)");
+    BANDLU_ARG(batch <= 1 || strideA >= lda * n, 4, "band_detect_batched: strideA < lda*n");
+    BANDLU_ARG(batch >= 0, 5, "band_detect_batched: batch < 0");
+    BANDLU_ARG(batch == 0 || d_out != nullptr, 8, "band_detect_batched: d_out is null");
+    BANDLU_ARG(d_max != nullptr, 9, "band_detect_batched: d_max is null");
+    BANDLU_ARG(n == 0 || batch == 0 || dA != nullptr, 1, "band_detect_batched: dA is null");
+    if (n > kMaxN || (n > 0 && batch > INT64_MAX / n)) {
+        set_error("band_detect_batched: sizes too large");
+        return BANDLU_ERR_UNSUPPORTED;
+    }
+    return launch_detect(dA, n, lda, strideA, batch, kl_cap, ku_cap, d_out, d_max,
+                         as_stream(stream));
+}

@@ -1,0 +1,276 @@
+// Step 3 of the structure-aware strategy (Sec. II-A cost f(N); Sec. III-A
+// banded LU, xGBTRF): kernel selection and the unblocked any-bandwidth kernel.
+//
+// Variants (band_getrf_variant):
+//   WINDOW      kl <= 31 and 2kl+ku+1 <= 128: register window, 64 lanes per
+//               matrix (getrf_window.hpp);
+//   WINDOW_G16  batched, kl <= 7 and 2kl+ku+1 <= 32: register window, 16
+//               lanes per matrix, four matrices per wavefront;
+//   GENERIC     everything else: one workgroup per matrix works on the band
+//               in global memory, one column step at a time.
+// All variants produce bitwise the factors of the unblocked algorithm.
+#include <cfloat>
+#include <climits>
+
+#include "getrf_window.hpp"
+
+namespace bandlu {
+
+WinKernel win_kernel_g64_c1_h1_8(int H);
+WinKernel win_kernel_g64_c1_h9_16(int H);
+WinKernel win_kernel_g64_c1_h17_24(int H);
+WinKernel win_kernel_g64_c1_h25_32(int H);
+WinKernel win_kernel_g64_c2_h1_8(int H);
+WinKernel win_kernel_g64_c2_h9_16(int H);
+WinKernel win_kernel_g64_c2_h17_24(int H);
+WinKernel win_kernel_g16_c1_h1_8(int H);
+WinKernel win_kernel_g16_c2_h1_8(int H);
+
+WinKernel win_kernel(int G, int CPL, int H) {
+    if (G == 16) {
+        if (H > 8) return nullptr;
+        return CPL == 1 ? win_kernel_g16_c1_h1_8(H) : win_kernel_g16_c2_h1_8(H);
+    }
+    if (CPL == 1) {
+        if (H <= 8) return win_kernel_g64_c1_h1_8(H);
+        if (H <= 16) return win_kernel_g64_c1_h9_16(H);
+        if (H <= 24) return win_kernel_g64_c1_h17_24(H);
+        return win_kernel_g64_c1_h25_32(H);
+    }
+    if (H <= 8) return win_kernel_g64_c2_h1_8(H);
+    if (H <= 16) return win_kernel_g64_c2_h9_16(H);
+    return win_kernel_g64_c2_h17_24(H);
+}
+
+namespace {
+
+constexpr int kGenThreads = 256;
+
+struct GenParams {
+    double *AB;
+    int32_t *ipiv;
+    int32_t *info;
+    int64_t n, kl, ku, ldab, strideAB, strideP;
+};
+
+// pivot key: |x|, with a NaN ranked first in position 0 and last elsewhere, so
+// that (largest key, smallest index) equals the BLAS i_amax choice
+__device__ inline double pivot_key(double x, int64_t t) {
+    if (__builtin_isnan(x)) return t == 0 ? __builtin_inf() : -1.0;
+    return fabs(x);
+}
+
+__device__ inline bool key_better(double ka, int64_t ia, double kb, int64_t ib) {
+    return ka > kb || (ka == kb && ia < ib);
+}
+
+__global__ __launch_bounds__(kGenThreads) void getrf_generic_kernel(GenParams P) {
+    const int64_t b = blockIdx.x;
+    double *__restrict__ AB = P.AB + b * P.strideAB;
+    int32_t *__restrict__ ipiv = P.ipiv + b * P.strideP;
+    const int64_t n = P.n, kl = P.kl, ku = P.ku, kv = kl + ku, ldab = P.ldab;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    __shared__ double s_key[kGenThreads / 64];
+    __shared__ int64_t s_idx[kGenThreads / 64];
+    __shared__ int64_t s_p;
+    __shared__ int s_nz;
+
+    // in-matrix fill slots start at zero
+    if (kl > 0) {
+        for (int64_t idx = tid; idx < n * kl; idx += kGenThreads) {
+            const int64_t c = idx / kl, r = idx - c * kl;
+            if (r >= kv - c) AB[c * ldab + r] = 0.0;
+        }
+    }
+    __syncthreads();
+
+    int64_t ju = 0;
+    int32_t info = 0;
+    for (int64_t j = 0; j < n; ++j) {
+        const int64_t km = min(kl, n - 1 - j);
+        double *colj = AB + j * ldab + kv;  // colj[t] = a(j+t, j)
+        double bk = -2.0;
+        int64_t bi = INT64_MAX;
+        for (int64_t t = tid; t <= km; t += kGenThreads) {
+            const double k = pivot_key(colj[t], t);
+            if (key_better(k, t, bk, bi)) { bk = k; bi = t; }
+        }
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) {
+            const double ok = __shfl_xor(bk, o, 64);
+            const int64_t oi = __shfl_xor(bi, o, 64);
+            if (key_better(ok, oi, bk, bi)) { bk = ok; bi = oi; }
+        }
+        if (lane == 0) { s_key[wv] = bk; s_idx[wv] = bi; }
+        __syncthreads();
+        if (tid == 0) {
+            double kk = s_key[0];
+            int64_t ii = s_idx[0];
+            for (int w = 1; w < kGenThreads / 64; ++w)
+                if (key_better(s_key[w], s_idx[w], kk, ii)) { kk = s_key[w]; ii = s_idx[w]; }
+            s_p = ii;
+            s_nz = colj[ii] != 0.0;
+            ipiv[j] = int32_t(j + ii + 1);
+        }
+        __syncthreads();
+        const int64_t p = s_p;
+        if (s_nz) {
+            ju = max(ju, min(j + ku + p, n - 1));
+            if (p != 0) {
+                for (int64_t c = j + tid; c <= ju; c += kGenThreads) {
+                    double *x = AB + c * ldab + (kv + j - c);
+                    const double t0 = x[0];
+                    x[0] = x[p];
+                    x[p] = t0;
+                }
+                __syncthreads();
+            }
+            const double piv = colj[0];
+            if (fabs(piv) >= DBL_MIN) {
+                const double rcp = 1.0 / piv;
+                for (int64_t t = 1 + tid; t <= km; t += kGenThreads) colj[t] = colj[t] * rcp;
+            } else {
+                for (int64_t t = 1 + tid; t <= km; t += kGenThreads) colj[t] = colj[t] / piv;
+            }
+            __syncthreads();
+            if (km > 0) {
+                const int64_t total = km * (ju - j);
+                for (int64_t idx = tid; idx < total; idx += kGenThreads) {
+                    const int64_t ci = idx / km, t = idx - ci * km + 1;
+                    const int64_t c = j + 1 + ci;
+                    double *x = AB + c * ldab + (kv + j - c);  // x[0] = a(j, c)
+                    x[t] = __builtin_fma(-colj[t], x[0], x[t]);
+                }
+            }
+            __syncthreads();
+        } else if (info == 0) {
+            info = int32_t(j + 1);
+        }
+    }
+    if (tid == 0) P.info[b] = info;
+}
+
+__global__ void zero_info_kernel(int32_t *info, int64_t batch) {
+    int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i < batch) info[i] = 0;
+}
+
+int select_variant(int64_t n, int64_t kl, int64_t ku, int64_t batch) {
+    const int64_t need = 2 * kl + ku + 1;
+    (void)n;
+    if (batch >= 64 && kl <= 7 && need <= 32) return BANDLU_GETRF_WINDOW_G16;
+    if (kl <= 31 && need <= 128 && (need <= 64 || kl <= 23)) return BANDLU_GETRF_WINDOW;
+    return BANDLU_GETRF_GENERIC;
+}
+
+int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
+                 int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info,
+                 int64_t batch, hipStream_t s) {
+    if (batch == 0) return BANDLU_OK;
+    if (n == 0) {
+        hipLaunchKernelGGL(zero_info_kernel, dim3((unsigned)((batch + 255) / 256)), dim3(256), 0,
+                           s, d_info, batch);
+        BANDLU_CHECK_LAUNCH("band_getrf (n = 0)");
+        return BANDLU_OK;
+    }
+    const int v = select_variant(n, kl, ku, batch);
+    const int64_t need = 2 * kl + ku + 1;
+    if (v == BANDLU_GETRF_WINDOW || v == BANDLU_GETRF_WINDOW_G16) {
+        WinParams W;
+        W.AB = dAB;
+        W.ipiv = d_ipiv;
+        W.info = d_info;
+        W.ldab = ldab;
+        W.strideAB = strideAB;
+        W.strideP = strideP;
+        W.n = (int)n;
+        W.ku = (int)ku;
+        W.batch = (int)batch;
+        const int H = (int)kl + 1;
+        WinKernel k;
+        int per_wave;
+        if (v == BANDLU_GETRF_WINDOW_G16) {
+            k = win_kernel(16, need <= 16 ? 1 : 2, H);
+            per_wave = 4;
+        } else {
+            k = win_kernel(64, need <= 64 ? 1 : 2, H);
+            per_wave = 1;
+        }
+        if (!k) {
+            set_error("band_getrf: no window kernel for kl = %lld", (long long)kl);
+            return BANDLU_ERR_UNSUPPORTED;
+        }
+        const int64_t blocks = (batch + per_wave - 1) / per_wave;
+        hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(64), 0, s, W);
+        BANDLU_CHECK_LAUNCH("band_getrf (window)");
+        return BANDLU_OK;
+    }
+    GenParams P;
+    P.AB = dAB;
+    P.ipiv = d_ipiv;
+    P.info = d_info;
+    P.n = n;
+    P.kl = kl;
+    P.ku = ku;
+    P.ldab = ldab;
+    P.strideAB = strideAB;
+    P.strideP = strideP;
+    hipLaunchKernelGGL(getrf_generic_kernel, dim3((unsigned)batch), dim3(kGenThreads), 0, s, P);
+    BANDLU_CHECK_LAUNCH("band_getrf (generic)");
+    return BANDLU_OK;
+}
+
+}  // namespace
+}  // namespace bandlu
+
+using namespace bandlu;
+
+extern "C" int band_getrf_variant(int64_t n, int64_t kl, int64_t ku, int64_t batch) {
+    const int64_t bmax = n > 1 ? n - 1 : 0;
+    if (n < 0) return -1;
+    if (kl < 0 || kl > bmax) return -2;
+    if (ku < 0 || ku > bmax) return -3;
+    if (batch < 0) return -4;
+    return select_variant(n, kl, ku, batch);
+}
+
+extern "C" int band_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
+                          int32_t *d_ipiv, int32_t *d_info, void *stream) {
+    clear_error();
+    const int64_t bmax = n > 1 ? n - 1 : 0;
+    BANDLU_ARG(n >= 0, 1, "band_getrf: n < 0");
+    BANDLU_ARG(kl >= 0 && kl <= bmax, 2, "band_getrf: kl out of [0, max(0, n-1)]");
+    BANDLU_ARG(ku >= 0 && ku <= bmax, 3, "band_getrf: ku out of [0, max(0, n-1)]");
+    BANDLU_ARG(n == 0 || dAB != nullptr, 4, "band_getrf: dAB is null");
+    BANDLU_ARG(ldab >= 2 * kl + ku + 1, 5, "band_getrf: ldab < 2kl+ku+1");
+    BANDLU_ARG(n == 0 || d_ipiv != nullptr, 6, "band_getrf: d_ipiv is null");
+    BANDLU_ARG(d_info != nullptr, 7, "band_getrf: d_info is null");
+    if (n > kMaxN) {
+        set_error("band_getrf: n >= 2^31 is not supported");
+        return BANDLU_ERR_UNSUPPORTED;
+    }
+    return launch_getrf(n, kl, ku, dAB, ldab, ldab * n, d_ipiv, n, d_info, 1, as_stream(stream));
+}
+
+extern "C" int band_getrf_batched(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
+                                  int64_t strideAB, int32_t *d_ipiv, int64_t strideP,
+                                  int32_t *d_info, int64_t batch, void *stream) {
+    clear_error();
+    const int64_t bmax = n > 1 ? n - 1 : 0;
+    BANDLU_ARG(n >= 0, 1, "band_getrf_batched: n < 0");
+    BANDLU_ARG(kl >= 0 && kl <= bmax, 2, "band_getrf_batched: kl out of range");
+    BANDLU_ARG(ku >= 0 && ku <= bmax, 3, "band_getrf_batched: ku out of range");
+    BANDLU_ARG(n == 0 || batch == 0 || dAB != nullptr, 4, "band_getrf_batched: dAB is null");
+    BANDLU_ARG(ldab >= 2 * kl + ku + 1, 5, "band_getrf_batched: ldab < 2kl+ku+1");
+    BANDLU_ARG(batch <= 1 || strideAB >= ldab * n, 6, "band_getrf_batched: strideAB < ldab*n");
+    BANDLU_ARG(n == 0 || batch == 0 || d_ipiv != nullptr, 7, "band_getrf_batched: d_ipiv is null");
+    BANDLU_ARG(batch <= 1 || strideP >= n, 8, "band_getrf_batched: strideP < n");
+    BANDLU_ARG(batch == 0 || d_info != nullptr, 9, "band_getrf_batched: d_info is null");
+    BANDLU_ARG(batch >= 0, 10, "band_getrf_batched: batch < 0");
+    if (n > kMaxN || batch > INT_MAX) {
+        set_error("band_getrf_batched: sizes too large");
+        return BANDLU_ERR_UNSUPPORTED;
+    }
+    return launch_getrf(n, kl, ku, dAB, ldab, strideAB, d_ipiv, strideP, d_info, batch,
+                        as_stream(stream));
+}

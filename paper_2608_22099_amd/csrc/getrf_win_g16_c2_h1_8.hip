@@ -1,0 +1,13 @@
+// Register-window banded LU instantiated for 16 lanes per matrix, 2 column(s)
+// per lane and kl + 1 = 1..8 (one file per range keeps compiles parallel).
+#include "getrf_window.hpp"
+
+namespace bandlu {
+
+WinKernel win_kernel_g16_c2_h1_8(int H) {
+    static constexpr auto table = WinRange<16, 2, 1, 8>::make(
+        std::make_integer_sequence<int, 8 - 1 + 1>{});
+    return (H >= 1 && H <= 8) ? table[H - 1] : nullptr;
+}
+
+}  // namespace bandlu

@@ -1,0 +1,299 @@
+"""GPU parity: every step of the HIP path against the CPU oracle on the same
+seeded inputs.  Bandwidths, band arrays, pivots and info must match bit for
+bit; the unblocked kernels also reproduce the factors and solutions bit for
+bit (the same operations in the same order), which is stricter than the
+1e-10 relative tolerance the method is held to."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_22099_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from paper_2608_22099_amd import bandlu  # noqa: E402  (loads libbandlu.so)
+
+DEV = "cuda:0"
+
+
+def to_dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+def bits(x):
+    return np.ascontiguousarray(x).view(np.uint64)
+
+
+def assert_bitwise(g, o, what):
+    g = np.ascontiguousarray(g)
+    o = np.ascontiguousarray(o)
+    assert g.shape == o.shape, (what, g.shape, o.shape)
+    bad = np.nonzero(bits(g) != bits(o))
+    assert bad[0].size == 0, f"{what}: {bad[0].size} mismatches, first at {tuple(b[0] for b in bad)}: gpu={g[tuple(b[0] for b in bad)]!r} oracle={o[tuple(b[0] for b in bad)]!r}"
+
+
+def gpu_pipeline(T, kl, ku, ldab=None):
+    """dense -> band -> getrf on the GPU; returns numpy (AB0, ABf, ipiv, info)."""
+    A = to_dev(T)
+    AB = bandlu.dense_to_band(A, kl, ku, ldab=ldab)
+    AB0 = AB.cpu().numpy()
+    ipiv, info = bandlu.band_getrf(AB, kl, ku)
+    torch.cuda.synchronize()
+    return AB0, AB.cpu().numpy(), ipiv.cpu().numpy(), int(info.cpu()[0])
+
+
+def oracle_pipeline(T, kl, ku, ldab=None):
+    n = T.shape[0]
+    ldab = ldab or 2 * kl + ku + 1
+    AB = np.zeros((n, ldab))
+    AB, _ = oracle.dense_to_band(T, kl, ku, ldab=ldab, AB=AB)
+    AB0 = AB.copy()
+    ipiv, info, _ = oracle.gbtrf(AB, kl, ku)
+    return AB0, AB, ipiv, info
+
+
+# ------------------------------------------------------------------ detect --
+@pytest.mark.parametrize("seed", range(24))
+def test_detect_random(seed):
+    T, _, _ = inputs.random_case(seed, n_max=300 if seed % 2 else 40, special=True,
+                                 lda_pad=seed % 3)
+    o = oracle.detect(T)
+    g = bandlu.band_detect(to_dev(T)).cpu().numpy()
+    assert tuple(g) == o[:3]
+
+
+def test_detect_special_values():
+    n = 70
+    for (i, j, v) in [(69, 0, np.nan), (0, 69, np.inf), (5, 2, 5e-324), (3, 60, -0.0)]:
+        T = np.zeros((n, n))
+        T[j, i] = v
+        o = oracle.detect(T)
+        g = bandlu.band_detect(to_dev(T)).cpu().numpy()
+        assert tuple(g) == o[:3], (i, j, v)
+    T = np.zeros((0, 1))
+    assert tuple(bandlu.band_detect(to_dev(T)).cpu().numpy()) == (0, 0, 0)
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 127, 128, 129, 255, 1000, 1023, 1025])
+def test_detect_odd_sizes_and_alignment(n):
+    rng = np.random.default_rng(n)
+    kl, ku = int(rng.integers(0, n)), int(rng.integers(0, n))
+    T = inputs.banded_dense(n, kl, ku, 7 + n, check=False)
+    for pad in (0, 1):
+        TT = np.zeros((n, n + pad))
+        TT[:, :n] = T
+        assert tuple(bandlu.band_detect(to_dev(TT)).cpu().numpy()) == oracle.detect(TT)[:3]
+
+
+def test_detect_caps():
+    T = inputs.banded_dense(2048, 40, 7, 3)
+    A = to_dev(T)
+    # caps at or above the true bandwidths: exact answer, no early exit
+    assert tuple(bandlu.band_detect(A, 40, 7).cpu().numpy()) == (40, 7, 0)
+    assert tuple(bandlu.band_detect(A, 100, 100).cpu().numpy()) == (40, 7, 0)
+    # caps below: exceeded, values are lower bounds with one above its cap
+    for kc, uc in [(39, -1), (-1, 6), (10, 3)]:
+        kl, ku, ex = bandlu.band_detect(A, kc, uc).cpu().numpy()
+        assert ex == 1 and kl <= 40 and ku <= 7
+        assert (kc >= 0 and kl > kc) or (uc >= 0 and ku > uc)
+
+
+def test_detect_batched():
+    batch, n = 37, 90
+    T = np.zeros((batch, n, n))
+    want = []
+    for b in range(batch):
+        rng = np.random.default_rng(b)
+        kl, ku = int(rng.integers(0, 12)), int(rng.integers(0, 12))
+        inputs.banded_dense(n, kl, ku, 100 + b, out=T[b], check=False)
+        want.append(oracle.detect(T[b])[:3])
+    out, dmax = bandlu.band_detect_batched(to_dev(T))
+    assert [tuple(r) for r in out.cpu().numpy()] == want
+    w = np.array(want)
+    assert tuple(dmax.cpu().numpy()) == (w[:, 0].max(), w[:, 1].max(), w[:, 2].max())
+    out, dmax = bandlu.band_detect_batched(to_dev(T), 5, -1)
+    o = out.cpu().numpy()
+    for b in range(batch):
+        assert o[b, 2] == int(want[b][0] > 5)
+        if o[b, 2] == 0:
+            assert tuple(o[b]) == want[b]
+
+
+# ----------------------------------------------------------------- convert --
+@pytest.mark.parametrize("seed", range(20))
+def test_convert_random(seed):
+    T, kl, ku = inputs.random_case(300 + seed, n_max=200, special=True, lda_pad=seed % 2)
+    n = T.shape[0]
+    ldab = 2 * kl + ku + 1 + seed % 3
+    AB = torch.full((n, ldab), float("nan"), dtype=torch.float64, device=DEV)
+    bandlu.dense_to_band(to_dev(T), kl, ku, AB=AB)
+    o, _ = oracle.dense_to_band(T, kl, ku, ldab=ldab)
+    assert_bitwise(AB.cpu().numpy(), o, "dense_to_band")
+
+
+def test_convert_batched():
+    batch, n, kl, ku = 50, 64, 5, 9
+    T = np.stack([inputs.banded_dense(n, kl, ku, b) for b in range(batch)])
+    AB = bandlu.dense_to_band_batched(to_dev(T), kl, ku).cpu().numpy()
+    for b in range(batch):
+        assert_bitwise(AB[b], oracle.dense_to_band(T[b], kl, ku)[0], f"batch {b}")
+
+
+# ------------------------------------------------------------------- getrf --
+def random_band(n, kl, ku, seed, shift=0.0):
+    return inputs.banded_dense(n, kl, ku, seed, shift=shift, check=False)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_getrf_random_shapes(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 200))
+    kl = int(rng.integers(0, min(n, 40)))
+    ku = int(rng.integers(0, min(n, 70)))
+    T = random_band(n, kl, ku, 9000 + seed)
+    g = gpu_pipeline(T, kl, ku)
+    o = oracle_pipeline(T, kl, ku)
+    variant = bandlu.band_getrf_variant(n, kl, ku)
+    assert np.array_equal(g[2], o[2]), f"ipiv ({variant})"
+    assert g[3] == o[3]
+    assert_bitwise(g[1], o[1], f"factors ({variant}, n={n}, kl={kl}, ku={ku})")
+
+
+@pytest.mark.parametrize("kl,ku", [(0, 0), (1, 0), (0, 1), (3, 3), (16, 16), (2, 64), (31, 3),
+                                   (23, 80), (8, 50), (5, 60), (24, 2)])
+def test_getrf_window_boundaries(kl, ku):
+    for n in (kl + ku + 1, 300):
+        n = max(n, max(kl, ku) + 1)
+        T = random_band(n, kl, ku, 77 + kl * 100 + ku)
+        g = gpu_pipeline(T, kl, ku)
+        o = oracle_pipeline(T, kl, ku)
+        assert np.array_equal(g[2], o[2]) and g[3] == o[3]
+        assert_bitwise(g[1], o[1], f"n={n} kl={kl} ku={ku}")
+
+
+def test_getrf_singular_and_nan():
+    n, kl, ku = 50, 3, 2
+    for k in [0, 7, 49]:
+        T = random_band(n, kl, ku, 5 + k)
+        T[k, :] = 0.0
+        g, o = gpu_pipeline(T, kl, ku), oracle_pipeline(T, kl, ku)
+        assert g[3] == o[3] == k + 1
+        assert np.array_equal(g[2], o[2])
+        assert_bitwise(g[1], o[1], "singular")
+    T = random_band(n, kl, ku, 99)
+    T[4, 4] = np.nan   # NaN on the diagonal: taken when first
+    T[10, 12] = np.nan  # NaN below the diagonal: never taken
+    g, o = gpu_pipeline(T, kl, ku), oracle_pipeline(T, kl, ku)
+    assert np.array_equal(g[2], o[2]) and g[3] == o[3]
+    assert_bitwise(g[1], o[1], "nan")
+    Z = np.zeros((20, 20))
+    g, o = gpu_pipeline(Z, 2, 3), oracle_pipeline(Z, 2, 3)
+    assert g[3] == 1 and np.array_equal(g[2], o[2])
+    assert_bitwise(g[1], o[1], "zero matrix")
+
+
+def test_getrf_tiny_pivots():
+    """|pivot| < DBL_MIN takes the division branch on both sides."""
+    n, kl, ku = 40, 2, 2
+    T = random_band(n, kl, ku, 5) * 1e-300
+    g, o = gpu_pipeline(T, kl, ku), oracle_pipeline(T, kl, ku)
+    assert np.array_equal(g[2], o[2])
+    assert_bitwise(g[1], o[1], "tiny")
+
+
+def test_getrf_fill_rows_not_read():
+    n, kl, ku = 100, 4, 3
+    T = random_band(n, kl, ku, 8)
+    A = to_dev(T)
+    AB = bandlu.dense_to_band(A, kl, ku)
+    AB[:, :kl] = float("nan")
+    ipiv, info = bandlu.band_getrf(AB, kl, ku)
+    o = oracle_pipeline(T, kl, ku)
+    got = AB.cpu().numpy()
+    kv = kl + ku
+    for j in range(n):  # slots outside the matrix keep what they held
+        for r in range(kl):
+            if r - kv + j < 0:
+                got[j, r] = 0.0
+    assert np.array_equal(ipiv.cpu().numpy(), o[2])
+    assert_bitwise(got, o[1], "fill rows")
+
+
+@pytest.mark.parametrize("kl,ku,batch,n", [(4, 4, 256, 64), (1, 2, 100, 33), (7, 3, 70, 50),
+                                           (4, 4, 3, 64), (10, 5, 65, 40), (3, 20, 64, 90)])
+def test_getrf_batched(kl, ku, batch, n):
+    T = np.stack([random_band(n, kl, ku, 500 + b) for b in range(batch)])
+    T[1 % batch, 3, :] = 0.0  # one singular matrix
+    A = to_dev(T)
+    AB = bandlu.dense_to_band_batched(A, kl, ku)
+    ipiv, info = bandlu.band_getrf_batched(AB, kl, ku)
+    ABg, ipg, infg = AB.cpu().numpy(), ipiv.cpu().numpy(), info.cpu().numpy()
+    for b in range(batch):
+        o = oracle_pipeline(T[b], kl, ku)
+        assert np.array_equal(ipg[b], o[2]) and infg[b] == o[3], b
+        assert_bitwise(ABg[b], o[1], f"batch {b}")
+
+
+def test_getrf_deterministic():
+    T = random_band(3000, 16, 16, 1)
+    a = gpu_pipeline(T, 16, 16)
+    b = gpu_pipeline(T, 16, 16)
+    assert_bitwise(a[1], b[1], "rerun")
+
+
+# ------------------------------------------------------------------- getrs --
+@pytest.mark.parametrize("seed", range(16))
+def test_getrs_random(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 300))
+    kl = int(rng.integers(0, min(n, 30)))
+    ku = int(rng.integers(0, min(n, 90)))
+    nrhs = int(rng.integers(1, 4))
+    T = random_band(n, kl, ku, 700 + seed, shift=4.0)
+    _, ABo, ipo, _ = oracle_pipeline(T, kl, ku)
+    B = rng.standard_normal((nrhs, n))
+    xo = oracle.gbtrs(ABo, kl, ku, ipo, B.copy())
+    Bg = to_dev(B)
+    bandlu.band_getrs(to_dev(ABo), kl, ku, to_dev(ipo), Bg)
+    assert_bitwise(Bg.cpu().numpy(), xo, f"getrs n={n} kl={kl} ku={ku}")
+
+
+def test_getrs_large_bands():
+    for n, kl, ku in [(700, 70, 100), (2000, 200, 300)]:
+        T = random_band(n, kl, ku, n, shift=float(kl + ku))
+        _, ABo, ipo, _ = oracle_pipeline(T, kl, ku)
+        B = np.random.default_rng(n).standard_normal((1, n))
+        xo = oracle.gbtrs(ABo, kl, ku, ipo, B.copy())
+        Bg = to_dev(B)
+        bandlu.band_getrs(to_dev(ABo), kl, ku, to_dev(ipo), Bg)
+        assert_bitwise(Bg.cpu().numpy(), xo, f"getrs n={n}")
+
+
+def test_getrs_global_path():
+    n, kl, ku = 9000, 3, 5  # right-hand side larger than the LDS path
+    T = random_band(n, kl, ku, 4, shift=10.0)
+    _, ABo, ipo, _ = oracle_pipeline(T, kl, ku)
+    B = np.random.default_rng(1).standard_normal((2, n))
+    xo = oracle.gbtrs(ABo, kl, ku, ipo, B.copy())
+    Bg = to_dev(B)
+    bandlu.band_getrs(to_dev(ABo), kl, ku, to_dev(ipo), Bg)
+    assert_bitwise(Bg.cpu().numpy(), xo, "getrs global")
+
+
+def test_getrs_batched():
+    batch, n, kl, ku, nrhs = 40, 80, 4, 4, 2
+    T = np.stack([random_band(n, kl, ku, 900 + b) for b in range(batch)])
+    outs = [oracle_pipeline(T[b], kl, ku) for b in range(batch)]
+    AB = np.stack([o[1] for o in outs])
+    ip = np.stack([o[2] for o in outs])
+    B = np.random.default_rng(3).standard_normal((batch, nrhs, n))
+    Bg = to_dev(B)
+    bandlu.band_getrs_batched(to_dev(AB), kl, ku, to_dev(ip), Bg)
+    got = Bg.cpu().numpy()
+    for b in range(batch):
+        xo = oracle.gbtrs(AB[b], kl, ku, ip[b], B[b].copy())
+        assert_bitwise(got[b], xo, f"batch {b}")

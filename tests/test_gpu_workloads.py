@@ -1,0 +1,79 @@
+"""GPU parity on the named workloads at their full sizes (the shapes the
+benchmark times): bandwidths, band arrays, pivots and info bit for bit, the
+factors and the solution bit for bit (unblocked kernels), and the backward
+error of the factorisation within the method's bound of 10."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_22099_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from paper_2608_22099_amd import bandlu  # noqa: E402
+
+DEV = "cuda:0"
+
+
+def bits(x):
+    return np.ascontiguousarray(x).view(np.uint64)
+
+
+@pytest.mark.parametrize("name", ["n1000_kl3_ku3", "n8192_kl16_ku16", "n16384_kl2_ku64"])
+def test_single_workload(name):
+    w = inputs.WORKLOADS[name]
+    n, kl, ku = w["n"], w["kl"], w["ku"]
+    T = inputs.workload_matrix(name)
+    A = torch.from_numpy(T).to(DEV)
+    det = bandlu.band_detect(A).cpu().numpy()
+    o = oracle.detect(T)
+    assert tuple(det) == o[:3] == (kl, ku, 0)
+    AB = bandlu.dense_to_band(A, kl, ku)
+    ABo, _ = oracle.dense_to_band(T, kl, ku)
+    assert np.array_equal(bits(AB.cpu().numpy()), bits(ABo))
+    del A
+    AB0 = ABo.copy()
+    ipiv, info = bandlu.band_getrf(AB, kl, ku)
+    ipo, info_o, _ = oracle.gbtrf(ABo, kl, ku)
+    assert np.array_equal(ipiv.cpu().numpy(), ipo) and int(info.cpu()[0]) == info_o == 0
+    ABg = AB.cpu().numpy()
+    assert np.array_equal(bits(ABg), bits(ABo))
+    assert oracle.band_backward_error(AB0, ABg, kl, ku, ipiv.cpu().numpy()) <= 10.0
+    b = inputs.workload_rhs(name)
+    xg = torch.from_numpy(b.copy()).to(DEV)
+    bandlu.band_getrs(AB, kl, ku, ipiv, xg)
+    xo = oracle.gbtrs(ABo, kl, ku, ipo, b.copy())
+    assert np.array_equal(bits(xg.cpu().numpy()), bits(xo))
+
+
+def test_batched_workload():
+    name = "batch4096_n256_kl4_ku4"
+    w = inputs.WORKLOADS[name]
+    n, kl, ku, batch = w["n"], w["kl"], w["ku"], w["batch"]
+    T = inputs.workload_batch(name)
+    A = torch.from_numpy(T).to(DEV)
+    out, dmax = bandlu.band_detect_batched(A)
+    out = out.cpu().numpy()
+    assert tuple(dmax.cpu().numpy()) == (kl, ku, 0)
+    sample = list(range(0, batch, 97)) + [batch - 1]
+    for b in sample:
+        assert tuple(out[b]) == oracle.detect(T[b])[:3]
+    AB = bandlu.dense_to_band_batched(A, kl, ku)
+    del A
+    ipiv, info = bandlu.band_getrf_batched(AB, kl, ku)
+    B = np.stack([inputs.workload_rhs(name, b) for b in range(batch)])
+    Bg = torch.from_numpy(B).to(DEV)
+    bandlu.band_getrs_batched(AB, kl, ku, ipiv, Bg)
+    ABg, ipg, infg, xg = AB.cpu().numpy(), ipiv.cpu().numpy(), info.cpu().numpy(), Bg.cpu().numpy()
+    assert np.all(infg == 0)
+    for b in sample:
+        ABo, _ = oracle.dense_to_band(T[b], kl, ku)
+        ipo, info_o, _ = oracle.gbtrf(ABo, kl, ku)
+        assert np.array_equal(ipg[b], ipo)
+        assert np.array_equal(bits(ABg[b]), bits(ABo))
+        xo = oracle.gbtrs(ABo, kl, ku, ipo, B[b].copy())
+        assert np.array_equal(bits(xg[b]), bits(xo))
