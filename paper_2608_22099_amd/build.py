@@ -11,6 +11,7 @@ from __future__ import annotations
 import argparse
 import concurrent.futures as cf
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -39,11 +40,25 @@ def sources():
 
 def _compile(src):
     obj = os.path.join(BUILD, os.path.basename(src)[:-4] + ".o")
-    cmd = [HIPCC, *CFLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *CFLAGS, "-Rpass-analysis=kernel-resource-usage", "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
-    return obj, r.stderr
+    # Every kernel must run without scratch memory: a register array indexed
+    # at run time or a spill would fall back to it, which is slow, and a large
+    # per-lane scratch size makes the runtime reserve memory for every wave slot.
+    fn, bad = None, []
+    for line in r.stderr.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            fn = m.group(1)
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and int(m.group(1)) > 0:
+            bad.append((fn, int(m.group(1))))
+    if bad:
+        raise RuntimeError(f"{src}: kernels use scratch memory: {bad[:5]}")
+    err = "\n".join(l for l in r.stderr.splitlines() if "remark:" not in l and "packed-fp32" not in l)
+    return obj, err
 
 
 def build(jobs: int | None = None, verbose: bool = False) -> str:

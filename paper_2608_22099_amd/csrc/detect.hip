@@ -137,6 +137,70 @@ __global__ __launch_bounds__(kThreads) void detect_kernel(DetectParams P) {
     if (j != 0) detect_flush(P, b, kl_l, ku_l, lane);
 }
 
+// Single contiguous matrix (lda == n, n even, n >= 2048): the matrix is one flat
+// stream of n*n doubles cut into 16 KiB chunks that consecutive workgroups
+// take in turn, so the whole chip reads one contiguous front of memory.  A
+// chunk spans at most two columns; n even keeps both doubles of a 16-byte load
+// in one column.
+constexpr int kFlatU = 4;
+constexpr int kFlatChunk = kThreads * 2 * kFlatU;  // doubles per chunk
+
+struct FlatParams {
+    const double *A;
+    int64_t n, total, nchunks;
+    int64_t kl_cap, ku_cap;
+    unsigned long long *out;
+};
+
+template <bool CAPS>
+__global__ __launch_bounds__(kThreads) void detect_flat_kernel(FlatParams P) {
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int n = int(P.n);
+    int kl_t = 0, ku_t = 0;
+    for (int64_t k = blockIdx.x; k < P.nchunks; k += gridDim.x) {
+        if (CAPS && __hip_atomic_load(P.out + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0ull)
+            break;
+        const int64_t f0 = k * kFlatChunk;
+        const int64_t col0 = f0 / P.n;
+        const int i0 = int(f0 - col0 * P.n);
+        const int c0 = int(col0);
+        const dbl2 *base = reinterpret_cast<const dbl2 *>(P.A + f0);
+        dbl2 v[kFlatU];
+#pragma unroll
+        for (int u = 0; u < kFlatU; ++u) {
+            const int e = u * (kThreads * 2) + tid * 2;
+            v[u] = f0 + e < P.total ? __builtin_nontemporal_load(base + (e >> 1)) : dbl2{0.0, 0.0};
+        }
+#pragma unroll
+        for (int u = 0; u < kFlatU; ++u) {
+            const int e = u * (kThreads * 2) + tid * 2;
+            int i = i0 + e, c = c0;
+            if (i >= n) { i -= n; ++c; }
+            const int d = i - c;
+            if (v[u].x != 0.0) { kl_t = max(kl_t, d); ku_t = max(ku_t, -d); }
+            if (v[u].y != 0.0) { kl_t = max(kl_t, d + 1); ku_t = max(ku_t, -d - 1); }
+        }
+        if (CAPS) {
+            const bool ex = (int64_t)kl_t > P.kl_cap || (int64_t)ku_t > P.ku_cap;
+            if (__any(ex) && lane == 0)
+                __hip_atomic_store(P.out + 2, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+    __shared__ int s_kl[kThreads / 64], s_ku[kThreads / 64];
+    kl_t = wave_max_i32(kl_t);
+    ku_t = wave_max_i32(ku_t);
+    if (lane == 0) { s_kl[tid >> 6] = kl_t; s_ku[tid >> 6] = ku_t; }
+    __syncthreads();
+    if (tid == 0) {
+        int a = 0, b = 0;
+        for (int w = 0; w < kThreads / 64; ++w) { a = max(a, s_kl[w]); b = max(b, s_ku[w]); }
+        if (a > 0) atomicMax(P.out + 0, (unsigned long long)a);
+        if (b > 0) atomicMax(P.out + 1, (unsigned long long)b);
+        if ((int64_t)a > P.kl_cap || (int64_t)b > P.ku_cap) atomicMax(P.out + 2, 1ull);
+    }
+}
+
 int launch_detect(const double *dA, int64_t n, int64_t lda, int64_t strideA, int64_t batch,
                   int64_t kl_cap, int64_t ku_cap, int64_t *d_out, int64_t *d_max,
                   hipStream_t s) {
@@ -150,6 +214,23 @@ int launch_detect(const double *dA, int64_t n, int64_t lda, int64_t strideA, int
         BANDLU_CHECK_LAUNCH("band_detect init");
     }
     if (n == 0 || batch == 0) return BANDLU_OK;
+    const bool caps = kl_cap >= 0 || ku_cap >= 0;
+    if (batch == 1 && lda == n && n % 2 == 0 && n >= 2048 &&
+        reinterpret_cast<uintptr_t>(dA) % 16 == 0) {
+        FlatParams F;
+        F.A = dA;
+        F.n = n;
+        F.total = n * n;
+        F.nchunks = (F.total + kFlatChunk - 1) / kFlatChunk;
+        F.kl_cap = kl_cap < 0 ? INT64_MAX : kl_cap;
+        F.ku_cap = ku_cap < 0 ? INT64_MAX : ku_cap;
+        F.out = reinterpret_cast<unsigned long long *>(d_out);
+        const int64_t grid = std::min<int64_t>(F.nchunks, int64_t(device_cu_count()) * 8);
+        hipLaunchKernelGGL(caps ? detect_flat_kernel<true> : detect_flat_kernel<false>,
+                           dim3((unsigned)grid), dim3(kThreads), 0, s, F);
+        BANDLU_CHECK_LAUNCH("band_detect (flat)");
+        return BANDLU_OK;
+    }
     DetectParams P;
     P.A = dA;
     P.n = n;
@@ -165,7 +246,6 @@ int launch_detect(const double *dA, int64_t n, int64_t lda, int64_t strideA, int
     P.ku_cap = ku_cap < 0 ? INT64_MAX : ku_cap;
     P.out = reinterpret_cast<unsigned long long *>(d_out);
     P.dmax = reinterpret_cast<unsigned long long *>(d_max);
-    const bool caps = kl_cap >= 0 || ku_cap >= 0;
     const bool vec = (reinterpret_cast<uintptr_t>(dA) % 16 == 0) && (lda % 2 == 0) &&
                      (batch == 1 || strideA % 2 == 0);
     auto k = vec ? (caps ? detect_kernel<true, true> : detect_kernel<true, false>)

@@ -2,8 +2,8 @@
 // banded LU, xGBTRF): kernel selection and the unblocked any-bandwidth kernel.
 //
 // Variants (band_getrf_variant):
-//   WINDOW      kl <= 31 and 2kl+ku+1 <= 128: register window, 64 lanes per
-//               matrix (getrf_window.hpp);
+//   WINDOW      kl <= 31 and 2kl+ku+1 <= 64, or kl <= 15 and 2kl+ku+1 <= 128:
+//               register window, 64 lanes per matrix (getrf_win64.hpp);
 //   WINDOW_G16  batched, kl <= 7 and 2kl+ku+1 <= 32: register window, 16
 //               lanes per matrix, four matrices per wavefront;
 //   GENERIC     everything else: one workgroup per matrix works on the band
@@ -12,6 +12,7 @@
 #include <cfloat>
 #include <climits>
 
+#include "bufio.hpp"
 #include "getrf_window.hpp"
 
 namespace bandlu {
@@ -22,7 +23,6 @@ WinKernel win_kernel_g64_c1_h17_24(int H);
 WinKernel win_kernel_g64_c1_h25_32(int H);
 WinKernel win_kernel_g64_c2_h1_8(int H);
 WinKernel win_kernel_g64_c2_h9_16(int H);
-WinKernel win_kernel_g64_c2_h17_24(int H);
 WinKernel win_kernel_g16_c1_h1_8(int H);
 WinKernel win_kernel_g16_c2_h1_8(int H);
 
@@ -39,7 +39,7 @@ WinKernel win_kernel(int G, int CPL, int H) {
     }
     if (H <= 8) return win_kernel_g64_c2_h1_8(H);
     if (H <= 16) return win_kernel_g64_c2_h9_16(H);
-    return win_kernel_g64_c2_h17_24(H);
+    return nullptr;
 }
 
 namespace {
@@ -159,7 +159,8 @@ int select_variant(int64_t n, int64_t kl, int64_t ku, int64_t batch) {
     const int64_t need = 2 * kl + ku + 1;
     (void)n;
     if (batch >= 64 && kl <= 7 && need <= 32) return BANDLU_GETRF_WINDOW_G16;
-    if (kl <= 31 && need <= 128 && (need <= 64 || kl <= 23)) return BANDLU_GETRF_WINDOW;
+    if (kl <= 31 && (need <= 64 || (need <= 128 && kl <= 15)) && need * n * 8 <= kMaxBufferBytes)
+        return BANDLU_GETRF_WINDOW;
     return BANDLU_GETRF_GENERIC;
 }
 
@@ -173,8 +174,11 @@ int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
         BANDLU_CHECK_LAUNCH("band_getrf (n = 0)");
         return BANDLU_OK;
     }
-    const int v = select_variant(n, kl, ku, batch);
+    int v = select_variant(n, kl, ku, batch);
     const int64_t need = 2 * kl + ku + 1;
+    // the single-matrix window kernel addresses the band through a range-checked
+    // buffer of at most 2 GiB
+    if (v == BANDLU_GETRF_WINDOW && ldab * n * 8 > kMaxBufferBytes) v = BANDLU_GETRF_GENERIC;
     if (v == BANDLU_GETRF_WINDOW || v == BANDLU_GETRF_WINDOW_G16) {
         WinParams W;
         W.AB = dAB;

@@ -8,6 +8,7 @@
 // D steps ahead into a register ring, so the step chain never waits on HBM.
 #include <algorithm>
 
+#include "bufio.hpp"
 #include "common.hpp"
 
 #include <utility>
@@ -23,6 +24,7 @@ struct RsParams {
 };
 
 constexpr int64_t kLdsMaxN = 8192;  // 64 KiB of LDS per right-hand side
+
 
 template <int W, int D, bool LDS>
 __global__ __launch_bounds__(64) void getrs_kernel(RsParams P) {
@@ -124,6 +126,144 @@ __global__ __launch_bounds__(64) void getrs_kernel(RsParams P) {
     }
 }
 
+// Register-window solve for narrow bands (kl <= 63, kl + ku < 64 * CPL).
+// Forward: row r of the right-hand side lives in lane r mod 64; at step j lane
+// j mod 64 holds b[j], the swap with row ipiv[j]-1 is an exchange between two
+// lanes, and lanes holding rows j+1..j+kl apply one fma each.  Backward: row r
+// lives in lane r mod 64, register sub-slot (r / 64) mod CPL; at step j the
+// lane holding b[j] divides by U(j,j) and lanes holding rows j-kl-ku..j-1 apply
+// one fma each.  Multipliers, U entries, pivot indices and rows entering the
+// window are loaded D steps ahead into register rings whose index is a
+// compile-time constant (the step loop is unrolled by 64 * CPL).  Every step is
+// straight-line code: memory goes through range-checked buffer operations and
+// lane predicates are selects, so the prefetch ring stays in flight.
+template <int CPL>
+__global__ __launch_bounds__(64) void getrs_win_kernel(RsParams P) {
+    constexpr int D = 16;
+    constexpr int M = 64 * CPL;
+    const int L = threadIdx.x;
+    const int64_t sys = blockIdx.x;
+    const int64_t bidx = sys / P.nrhs, k = sys - bidx * P.nrhs;
+    const int n = int(P.n), kl = int(P.kl), kv = int(P.kl + P.ku), ldab = int(P.ldab);
+    const Buf ab = make_buf(P.AB + bidx * P.strideAB, uint32_t(int64_t(ldab) * n * 8));
+    const Buf pb = make_buf(P.ipiv + bidx * P.strideP, uint32_t(int64_t(n) * 4));
+    const Buf xb = make_buf(P.B + bidx * P.strideB + k * P.ldb, uint32_t(int64_t(n) * 8));
+    auto rowoff = [](int r) -> uint32_t { return uint32_t(r) * 8u; };  // r < 0 or r >= n: outside
+
+    // ------------------------------------------------------------ forward --
+    if (kl > 0 && n > 1) {
+        double bv = buf_ld(xb, L <= kl ? rowoff(L) : kOutside);
+        auto loff = [&](int j) -> uint32_t {  // multiplier for this lane's row at step j
+            const int t = (L - j) & 63;
+            const bool ok = j < n - 1 && t >= 1 && t <= min(kl, n - 1 - j);
+            return ok ? uint32_t(j * ldab + kv + t) * 8u : kOutside;
+        };
+        double lr[D], rr[D];
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+            lr[d] = buf_ld(ab, loff(d));
+            rr[d] = buf_ld(xb, rowoff(kl + 1 + d));
+        }
+        int ipv = buf_ld_i32(pb, uint32_t(L) * 4u);
+        int ipv_next = buf_ld_i32(pb, uint32_t(L + 64) * 4u);
+        for (int j0 = 0; j0 < n - 1; j0 += 64) {
+            [&]<int... Us>(std::integer_sequence<int, Us...>) {
+                (
+                    [&] {
+                        constexpr int u = Us;
+                        const int j = j0 + u;
+                        const bool live = j < n - 1;
+                        int l = __builtin_amdgcn_readlane(ipv, u) - 1;
+                        l = (live && l > j && l <= j + kl && l < n) ? l : j;
+                        if (l != j) {
+                            const int ls = l & 63;
+                            const double vj = readlane_d(bv, u);
+                            const double vl = readlane_d(bv, ls);
+                            bv = L == u ? vl : (L == ls ? vj : bv);
+                        }
+                        const double bj = readlane_d(bv, u);
+                        const int t = (L - u) & 63;
+                        const bool m = t >= 1 && t <= min(kl, n - 1 - j);
+                        const double nb = __builtin_fma(-lr[u % D], bj, bv);
+                        bv = m ? nb : bv;
+                        buf_st(xb, (L == u && live) ? rowoff(j) : kOutside, bv);  // row j is final
+                        const int renter = j + kl + 1;
+                        bv = (live && L == (renter & 63) && renter < n) ? rr[u % D] : bv;
+                        lr[u % D] = buf_ld(ab, loff(j + D));
+                        rr[u % D] = buf_ld(xb, rowoff(renter + D));
+                        if constexpr (u == 63) {
+                            ipv = ipv_next;
+                            ipv_next = buf_ld_i32(pb, uint32_t(j0 + 128 + L) * 4u);
+                        }
+                    }(),
+                    ...);
+            }(std::make_integer_sequence<int, 64>{});
+        }
+        buf_st(xb, L == ((n - 1) & 63) ? rowoff(n - 1) : kOutside, bv);
+        __threadfence();
+    }
+    // ----------------------------------------------------------- backward --
+    {
+        auto rowof = [&](int s, int j) -> int { return j - ((j - (L + 64 * s)) & (M - 1)); };
+        double bv[CPL];
+#pragma unroll
+        for (int s = 0; s < CPL; ++s) {
+            const int r = rowof(s, n - 1);
+            bv[s] = buf_ld(xb, r >= n - 1 - kv ? rowoff(r) : kOutside);
+        }
+        auto uoff = [&](int s, int j) -> uint32_t {  // U(row, j) for this lane's row at step j
+            const int t = j - rowof(s, j);
+            const bool ok = j >= 0 && t >= 1 && t <= min(kv, j);
+            return ok ? uint32_t(j * ldab + kv - t) * 8u : kOutside;
+        };
+        auto doff = [&](int j) -> uint32_t { return j >= 0 ? uint32_t(j * ldab + kv) * 8u : kOutside; };
+        double ur[CPL][D], dr[D], rr[D];
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+#pragma unroll
+            for (int s = 0; s < CPL; ++s) ur[s][d] = buf_ld(ab, uoff(s, n - 1 - d));
+            dr[d] = buf_ld(ab, doff(n - 1 - d));
+            rr[d] = buf_ld(xb, rowoff(n - 2 - kv - d));
+        }
+        // steps are counted from the end so that register indices are constants
+        for (int m0 = 0; m0 < n; m0 += M) {
+            [&]<int... Us>(std::integer_sequence<int, Us...>) {
+                (
+                    [&] {
+                        constexpr int u = Us;
+                        const int j = n - 1 - (m0 + u);
+                        const bool live = j >= 0;
+                        const int lj = j & 63;
+                        const int sj = (j >> 6) & (CPL - 1);
+                        double zs = bv[0];
+#pragma unroll
+                        for (int s = 1; s < CPL; ++s) zs = sj == s ? bv[s] : zs;
+                        const double z = zs / dr[u % D];
+                        const double xj = readlane_d(z, lj);
+                        buf_st(xb, (live && L == lj) ? rowoff(j) : kOutside, xj);
+#pragma unroll
+                        for (int s = 0; s < CPL; ++s) {
+                            const int t = j - rowof(s, j);
+                            const bool m = t >= 1 && t <= min(kv, j);
+                            const double nb = __builtin_fma(-ur[s][u % D], xj, bv[s]);
+                            bv[s] = m ? nb : bv[s];
+                        }
+                        const int renter = j - 1 - kv;
+                        const bool ent = live && renter >= 0 && L == (renter & 63);
+                        const int se = (renter >> 6) & (CPL - 1);
+#pragma unroll
+                        for (int s = 0; s < CPL; ++s) bv[s] = (ent && se == s) ? rr[u % D] : bv[s];
+#pragma unroll
+                        for (int s = 0; s < CPL; ++s) ur[s][u % D] = buf_ld(ab, uoff(s, j - D));
+                        dr[u % D] = buf_ld(ab, doff(j - D));
+                        rr[u % D] = buf_ld(xb, rowoff(renter - D));
+                    }(),
+                    ...);
+            }(std::make_integer_sequence<int, M>{});
+        }
+    }
+}
+
 template <int W>
 constexpr int rs_depth() { return W >= 16 ? 2 : 32 / W; }
 
@@ -162,6 +302,17 @@ int launch_getrs(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *
     if (systems > INT32_MAX) {
         set_error("band_getrs: batch * nrhs too large");
         return BANDLU_ERR_UNSUPPORTED;
+    }
+    const bool buf_ok = ldab * n * 8 <= kMaxBufferBytes && n * 8 <= kMaxBufferBytes;
+    if (buf_ok && kl <= 63 && kl + ku < 64) {
+        hipLaunchKernelGGL(getrs_win_kernel<1>, dim3((unsigned)systems), dim3(64), 0, s, P);
+        BANDLU_CHECK_LAUNCH("band_getrs (window)");
+        return BANDLU_OK;
+    }
+    if (buf_ok && kl <= 63 && kl + ku < 128) {
+        hipLaunchKernelGGL(getrs_win_kernel<2>, dim3((unsigned)systems), dim3(64), 0, s, P);
+        BANDLU_CHECK_LAUNCH("band_getrs (window)");
+        return BANDLU_OK;
     }
     const int64_t lanes_needed = std::max(kl, kl + ku + 1);
     const bool lds = n <= kLdsMaxN;

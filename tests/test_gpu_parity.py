@@ -28,11 +28,17 @@ def bits(x):
     return np.ascontiguousarray(x).view(np.uint64)
 
 
-def assert_bitwise(g, o, what):
+def assert_bitwise(g, o, what, nan_payload=False):
+    """Bitwise equality.  A NaN that arithmetic produced may carry any payload
+    (IEEE 754 leaves it open, and x86 and gfx950 differ), so unless
+    nan_payload is set, two NaNs in the same slot count as equal."""
     g = np.ascontiguousarray(g)
     o = np.ascontiguousarray(o)
     assert g.shape == o.shape, (what, g.shape, o.shape)
-    bad = np.nonzero(bits(g) != bits(o))
+    diff = bits(g) != bits(o)
+    if not nan_payload:
+        diff &= ~(np.isnan(g) & np.isnan(o))
+    bad = np.nonzero(diff)
     assert bad[0].size == 0, f"{what}: {bad[0].size} mismatches, first at {tuple(b[0] for b in bad)}: gpu={g[tuple(b[0] for b in bad)]!r} oracle={o[tuple(b[0] for b in bad)]!r}"
 
 
@@ -132,7 +138,7 @@ def test_convert_random(seed):
     AB = torch.full((n, ldab), float("nan"), dtype=torch.float64, device=DEV)
     bandlu.dense_to_band(to_dev(T), kl, ku, AB=AB)
     o, _ = oracle.dense_to_band(T, kl, ku, ldab=ldab)
-    assert_bitwise(AB.cpu().numpy(), o, "dense_to_band")
+    assert_bitwise(AB.cpu().numpy(), o, "dense_to_band", nan_payload=True)
 
 
 def test_convert_batched():
