@@ -39,11 +39,17 @@ constexpr int64_t kMaxN = (int64_t(1) << 31) - 1;
 int device_cu_count();
 
 // ---------------------------------------------------------------- device --
-// Wave-wide reductions for 64-lane wavefronts (gfx9 wave64).
+// Wave-wide max for 64-lane wavefronts (gfx9 wave64), uniform result: DPP
+// moves inside rows of 16 lanes (no LDS round trips), then the four row maxima
+// combined through scalar registers.
 __device__ inline int wave_max_i32(int v) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
-    return v;
+    v = max(v, __builtin_amdgcn_mov_dpp(v, 0xB1, 0xf, 0xf, false));   // quad_perm [1,0,3,2]
+    v = max(v, __builtin_amdgcn_mov_dpp(v, 0x4E, 0xf, 0xf, false));   // quad_perm [2,3,0,1]
+    v = max(v, __builtin_amdgcn_mov_dpp(v, 0x141, 0xf, 0xf, false));  // row_half_mirror
+    v = max(v, __builtin_amdgcn_mov_dpp(v, 0x140, 0xf, 0xf, false));  // row_mirror
+    const int a = max(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 16));
+    const int b = max(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48));
+    return max(a, b);
 }
 
 }  // namespace bandlu

@@ -38,20 +38,57 @@ __global__ void detect_init(unsigned long long *out, int64_t count, unsigned lon
     if (dmax && blockIdx.x == 0 && threadIdx.x < 3) dmax[threadIdx.x] = 0ull;
 }
 
+// Batch maximum of the per-matrix results (one workgroup).
+__global__ __launch_bounds__(kThreads) void detect_batch_max(const unsigned long long *out,
+                                                             int64_t batch, unsigned long long *dmax) {
+    int m0 = 0, m1 = 0, m2 = 0;
+    for (int64_t b = threadIdx.x; b < batch; b += kThreads) {
+        m0 = max(m0, int(out[3 * b + 0]));
+        m1 = max(m1, int(out[3 * b + 1]));
+        m2 = max(m2, int(out[3 * b + 2]));
+    }
+    __shared__ int s[3][kThreads / 64];
+    m0 = wave_max_i32(m0);
+    m1 = wave_max_i32(m1);
+    m2 = wave_max_i32(m2);
+    if ((threadIdx.x & 63) == 0) {
+        s[0][threadIdx.x >> 6] = m0;
+        s[1][threadIdx.x >> 6] = m1;
+        s[2][threadIdx.x >> 6] = m2;
+    }
+    __syncthreads();
+    if (threadIdx.x < 3) {
+        int m = 0;
+        for (int w = 0; w < kThreads / 64; ++w) m = max(m, s[threadIdx.x][w]);
+        dmax[threadIdx.x] = (unsigned long long)m;
+    }
+}
+
+// Raise *p to v.  Atomics on one address serialise in L2, and most
+// workgroups hold a value that is already published, so read first and issue
+// the atomic only when it can change the result.
+__device__ inline bool publish_max(unsigned long long *p, unsigned long long v) {
+    if (v > __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+        atomicMax(p, v);
+        return true;
+    }
+    return false;
+}
+
 // Publish the wave's bandwidths of matrix b.
 __device__ inline void detect_flush(const DetectParams &P, int64_t b, int kl_l, int ku_l, int lane) {
     int kl_w = wave_max_i32(kl_l);
     int ku_w = wave_max_i32(ku_l);
     if (lane == 0) {
         unsigned long long *o = P.out + 3 * b;
-        if (kl_w > 0) atomicMax(o + 0, (unsigned long long)kl_w);
-        if (ku_w > 0) atomicMax(o + 1, (unsigned long long)ku_w);
-        bool ex = (int64_t)kl_w > P.kl_cap || (int64_t)ku_w > P.ku_cap;
-        if (ex) atomicMax(o + 2, 1ull);
+        const bool r0 = publish_max(o + 0, (unsigned long long)kl_w);
+        const bool r1 = publish_max(o + 1, (unsigned long long)ku_w);
+        const bool ex = (int64_t)kl_w > P.kl_cap || (int64_t)ku_w > P.ku_cap;
+        const bool r2 = ex && publish_max(o + 2, 1ull);
         if (P.dmax) {
-            if (kl_w > 0) atomicMax(P.dmax + 0, (unsigned long long)kl_w);
-            if (ku_w > 0) atomicMax(P.dmax + 1, (unsigned long long)ku_w);
-            if (ex) atomicMax(P.dmax + 2, 1ull);
+            if (r0) publish_max(P.dmax + 0, (unsigned long long)kl_w);
+            if (r1) publish_max(P.dmax + 1, (unsigned long long)ku_w);
+            if (r2) publish_max(P.dmax + 2, 1ull);
         }
     }
 }
@@ -137,33 +174,44 @@ __global__ __launch_bounds__(kThreads) void detect_kernel(DetectParams P) {
     if (j != 0) detect_flush(P, b, kl_l, ku_l, lane);
 }
 
-// Single contiguous matrix (lda == n, n even, n >= 2048): the matrix is one flat
-// stream of n*n doubles cut into 16 KiB chunks that consecutive workgroups
-// take in turn, so the whole chip reads one contiguous front of memory.  A
-// chunk spans at most two columns; n even keeps both doubles of a 16-byte load
-// in one column.
-constexpr int kFlatU = 4;
+// Contiguous matrices (lda == n): the data is one flat stream cut into 32 KiB
+// chunks that consecutive workgroups take in turn, so the whole chip reads one
+// contiguous front of memory.
+//   single matrix (BATCHED = false): n even and >= 2048, so a chunk spans at
+//     most three columns; maxima are kept across chunks and published once;
+//   batch (BATCHED = true): n a power of two with n*n a multiple of the chunk,
+//     so a chunk lies in one matrix; each wave publishes per chunk.
+// n even keeps both doubles of a 16-byte load in one column.
+constexpr int kFlatU = 8;
 constexpr int kFlatChunk = kThreads * 2 * kFlatU;  // doubles per chunk
 
 struct FlatParams {
     const double *A;
     int64_t n, total, nchunks;
     int64_t kl_cap, ku_cap;
-    unsigned long long *out;
+    unsigned long long *out;   // [3 * batch]
+    unsigned long long *dmax;  // [3] (batched) or null
+    int64_t chunks_per_matrix; // batched: n*n / kFlatChunk
+    int log2n;                 // batched: n = 2^log2n
 };
 
-template <bool CAPS>
+template <bool CAPS, bool BATCHED>
 __global__ __launch_bounds__(kThreads) void detect_flat_kernel(FlatParams P) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int n = int(P.n);
     int kl_t = 0, ku_t = 0;
     for (int64_t k = blockIdx.x; k < P.nchunks; k += gridDim.x) {
-        if (CAPS && __hip_atomic_load(P.out + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0ull)
+        const int64_t mat = BATCHED ? k / P.chunks_per_matrix : 0;
+        unsigned long long *out = P.out + 3 * mat;
+        if (CAPS && __hip_atomic_load(out + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0ull) {
+            if (BATCHED) continue;
             break;
+        }
         const int64_t f0 = k * kFlatChunk;
-        const int64_t col0 = f0 / P.n;
-        const int i0 = int(f0 - col0 * P.n);
+        const int64_t fm = BATCHED ? f0 - mat * P.n * P.n : f0;  // offset inside the matrix
+        const int64_t col0 = BATCHED ? (fm >> P.log2n) : fm / P.n;
+        const int i0 = int(fm - col0 * P.n);
         const int c0 = int(col0);
         const dbl2 *base = reinterpret_cast<const dbl2 *>(P.A + f0);
         dbl2 v[kFlatU];
@@ -176,17 +224,36 @@ __global__ __launch_bounds__(kThreads) void detect_flat_kernel(FlatParams P) {
         for (int u = 0; u < kFlatU; ++u) {
             const int e = u * (kThreads * 2) + tid * 2;
             int i = i0 + e, c = c0;
-            if (i >= n) { i -= n; ++c; }
+            if (BATCHED) {
+                c += i >> P.log2n;
+                i &= n - 1;
+            } else {
+                while (i >= n) {  // n >= 2048: at most two wraps per 4096-element chunk
+                    i -= n;
+                    ++c;
+                }
+            }
             const int d = i - c;
             if (v[u].x != 0.0) { kl_t = max(kl_t, d); ku_t = max(ku_t, -d); }
             if (v[u].y != 0.0) { kl_t = max(kl_t, d + 1); ku_t = max(ku_t, -d - 1); }
         }
-        if (CAPS) {
+        if (BATCHED) {
+            const int a = wave_max_i32(kl_t), b = wave_max_i32(ku_t);
+            if (lane == 0) {
+                // non-returning atomics: the wave goes on to its next chunk
+                // without waiting; the batch maximum is formed afterwards
+                if (a > 0) atomicMax(out + 0, (unsigned long long)a);
+                if (b > 0) atomicMax(out + 1, (unsigned long long)b);
+                if ((int64_t)a > P.kl_cap || (int64_t)b > P.ku_cap) atomicMax(out + 2, 1ull);
+            }
+            kl_t = ku_t = 0;
+        } else if (CAPS) {
             const bool ex = (int64_t)kl_t > P.kl_cap || (int64_t)ku_t > P.ku_cap;
             if (__any(ex) && lane == 0)
-                __hip_atomic_store(P.out + 2, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(out + 2, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
+    if (BATCHED) return;
     __shared__ int s_kl[kThreads / 64], s_ku[kThreads / 64];
     kl_t = wave_max_i32(kl_t);
     ku_t = wave_max_i32(ku_t);
@@ -195,9 +262,9 @@ __global__ __launch_bounds__(kThreads) void detect_flat_kernel(FlatParams P) {
     if (tid == 0) {
         int a = 0, b = 0;
         for (int w = 0; w < kThreads / 64; ++w) { a = max(a, s_kl[w]); b = max(b, s_ku[w]); }
-        if (a > 0) atomicMax(P.out + 0, (unsigned long long)a);
-        if (b > 0) atomicMax(P.out + 1, (unsigned long long)b);
-        if ((int64_t)a > P.kl_cap || (int64_t)b > P.ku_cap) atomicMax(P.out + 2, 1ull);
+        publish_max(P.out + 0, (unsigned long long)a);
+        publish_max(P.out + 1, (unsigned long long)b);
+        if ((int64_t)a > P.kl_cap || (int64_t)b > P.ku_cap) publish_max(P.out + 2, 1ull);
     }
 }
 
@@ -215,20 +282,35 @@ int launch_detect(const double *dA, int64_t n, int64_t lda, int64_t strideA, int
     }
     if (n == 0 || batch == 0) return BANDLU_OK;
     const bool caps = kl_cap >= 0 || ku_cap >= 0;
-    if (batch == 1 && lda == n && n % 2 == 0 && n >= 2048 &&
-        reinterpret_cast<uintptr_t>(dA) % 16 == 0) {
+    const bool aligned = reinterpret_cast<uintptr_t>(dA) % 16 == 0;
+    int log2n = 0;
+    while ((int64_t(1) << log2n) < n) ++log2n;
+    const bool single_flat = batch == 1 && lda == n && n % 2 == 0 && n >= 2048 && aligned;
+    const bool batch_flat = batch > 1 && lda == n && strideA == n * n && (int64_t(1) << log2n) == n &&
+                            (n * n) % kFlatChunk == 0 && aligned;
+    if (single_flat || batch_flat) {
         FlatParams F;
         F.A = dA;
         F.n = n;
-        F.total = n * n;
+        F.total = n * n * batch;
         F.nchunks = (F.total + kFlatChunk - 1) / kFlatChunk;
         F.kl_cap = kl_cap < 0 ? INT64_MAX : kl_cap;
         F.ku_cap = ku_cap < 0 ? INT64_MAX : ku_cap;
         F.out = reinterpret_cast<unsigned long long *>(d_out);
+        F.dmax = reinterpret_cast<unsigned long long *>(d_max);
+        F.chunks_per_matrix = (n * n) / kFlatChunk;
+        F.log2n = log2n;
         const int64_t grid = std::min<int64_t>(F.nchunks, int64_t(device_cu_count()) * 8);
-        hipLaunchKernelGGL(caps ? detect_flat_kernel<true> : detect_flat_kernel<false>,
-                           dim3((unsigned)grid), dim3(kThreads), 0, s, F);
+        auto k = single_flat ? (caps ? detect_flat_kernel<true, false> : detect_flat_kernel<false, false>)
+                             : (caps ? detect_flat_kernel<true, true> : detect_flat_kernel<false, true>);
+        hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(kThreads), 0, s, F);
         BANDLU_CHECK_LAUNCH("band_detect (flat)");
+        if (batch_flat) {
+            hipLaunchKernelGGL(detect_batch_max, dim3(1), dim3(kThreads), 0, s,
+                               reinterpret_cast<const unsigned long long *>(d_out), batch,
+                               reinterpret_cast<unsigned long long *>(d_max));
+            BANDLU_CHECK_LAUNCH("band_detect (batch max)");
+        }
         return BANDLU_OK;
     }
     DetectParams P;

@@ -6,9 +6,13 @@
 //               register window, 64 lanes per matrix (getrf_win64.hpp);
 //   WINDOW_G16  batched, kl <= 7 and 2kl+ku+1 <= 32: register window, 16
 //               lanes per matrix, four matrices per wavefront;
-//   GENERIC     everything else: one workgroup per matrix works on the band
-//               in global memory, one column step at a time.
-// All variants produce bitwise the factors of the unblocked algorithm.
+//   BLOCKED     everything else with kl <= 256: panels of 32 columns factored
+//               in LDS, trailing band updated by many workgroups
+//               (getrf_blocked.hip);
+//   GENERIC     kl > 256: one workgroup per matrix works on the band in global
+//               memory, one column step at a time.
+// The window, blocked-exact and generic kernels produce bitwise the factors of
+// the unblocked algorithm on finite data.
 #include <cfloat>
 #include <climits>
 
@@ -41,6 +45,10 @@ WinKernel win_kernel(int G, int CPL, int H) {
     if (H <= 16) return win_kernel_g64_c2_h9_16(H);
     return nullptr;
 }
+
+int launch_getrf_blocked(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
+                         int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info,
+                         int64_t batch, bool use_mfma, hipStream_t s);
 
 namespace {
 
@@ -161,6 +169,7 @@ int select_variant(int64_t n, int64_t kl, int64_t ku, int64_t batch) {
     if (batch >= 64 && kl <= 7 && need <= 32) return BANDLU_GETRF_WINDOW_G16;
     if (kl <= 31 && (need <= 64 || (need <= 128 && kl <= 15)) && need * n * 8 <= kMaxBufferBytes)
         return BANDLU_GETRF_WINDOW;
+    if (kl <= 256 && n <= INT32_MAX && batch <= 65535) return BANDLU_GETRF_BLOCKED;
     return BANDLU_GETRF_GENERIC;
 }
 
@@ -209,6 +218,9 @@ int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
         BANDLU_CHECK_LAUNCH("band_getrf (window)");
         return BANDLU_OK;
     }
+    if (v == BANDLU_GETRF_BLOCKED)
+        return launch_getrf_blocked(n, kl, ku, dAB, ldab, strideAB, d_ipiv, strideP, d_info, batch,
+                                    false, s);
     GenParams P;
     P.AB = dAB;
     P.ipiv = d_ipiv;

@@ -147,17 +147,24 @@ __global__ __launch_bounds__(64) void getrf_win64_kernel(WinParams P) {
         double x = 0.0;     // TR: row j+L of column j
         if constexpr (H > 1) {
             if constexpr (TR) {
+                // the pivot lane writes its register elements in element order
+                // (consecutive registers, wide LDS stores); lane t reads the
+                // element of row j+t, i.e. element (S0 + t) mod H
                 if (L == src) {
 #pragma unroll
-                    for (int t = 0; t < H; ++t) {
-                        double v = a[0].get((S0 + t) % H);
+                    for (int k = 0; k < H; ++k) {
+                        double v = a[0].get(k);
 #pragma unroll
-                        for (int s = 1; s < CPL; ++s) v = sj == s ? a[s].get((S0 + t) % H) : v;
-                        s_col[t] = v;
+                        for (int s = 1; s < CPL; ++s) v = sj == s ? a[s].get(k) : v;
+                        s_col[k] = v;
                     }
                 }
                 __builtin_amdgcn_wave_barrier();
-                x = s_col[L & 31];
+                {
+                    const int t = L & 31;
+                    const int k = S0 + t < H ? S0 + t : S0 + t - H;
+                    x = s_col[k < H ? k : 0];
+                }
                 double key = __builtin_isnan(x) ? (L == 0 ? __builtin_inf() : -1.0) : fabs(x);
                 key = L <= km ? key : -2.0;
                 double kmax = row_max16<H>(key);
@@ -166,7 +173,7 @@ __global__ __launch_bounds__(64) void getrf_win64_kernel(WinParams P) {
                     kmax = fmax(k0, k1);
                 }
                 const unsigned long long hit = __ballot(key == kmax);
-                p = __builtin_ctzll(hit);
+                p = __builtin_amdgcn_readfirstlane(__builtin_ctzll(hit));
                 piv0 = readlane_d(x, p);
             } else {
                 double best = 0.0, bv = 0.0;
@@ -249,11 +256,13 @@ __global__ __launch_bounds__(64) void getrf_win64_kernel(WinParams P) {
                 // ---- 4. rank-1 update of columns j+1..ju
 #pragma unroll
                 for (int s = 0; s < CPL; ++s) {
-                    if (c[s] > j && c[s] <= ju) {
-                        const double u = a[s].get(S0);
+                    const bool m = c[s] > j && c[s] <= ju;
+                    const double u = a[s].get(S0);
 #pragma unroll
-                        for (int t = 1; t < H; ++t)
-                            a[s].set((S0 + t) % H, __builtin_fma(-Lm[t], u, a[s].get((S0 + t) % H)));
+                    for (int t = 1; t < H; ++t) {
+                        const double v = a[s].get((S0 + t) % H);
+                        const double nv = __builtin_fma(-Lm[t], u, v);
+                        a[s].set((S0 + t) % H, m ? nv : v);
                     }
                 }
             }

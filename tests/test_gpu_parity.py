@@ -303,3 +303,27 @@ def test_getrs_batched():
     for b in range(batch):
         xo = oracle.gbtrs(AB[b], kl, ku, ip[b], B[b].copy())
         assert_bitwise(got[b], xo, f"batch {b}")
+
+
+# ----------------------------------------------------------- blocked getrf --
+@pytest.mark.parametrize("n,kl,ku", [(300, 40, 3), (95, 20, 52), (700, 100, 150), (1100, 256, 256),
+                                     (530, 33, 200), (64, 63, 63), (257, 32, 0), (400, 250, 1)])
+def test_getrf_blocked_exact(n, kl, ku):
+    assert bandlu.band_getrf_variant(n, kl, ku) == "blocked"
+    T = random_band(n, kl, ku, 31 * n + kl)
+    g, o = gpu_pipeline(T, kl, ku), oracle_pipeline(T, kl, ku)
+    assert np.array_equal(g[2], o[2]) and g[3] == o[3]
+    assert_bitwise(g[1], o[1], f"blocked n={n} kl={kl} ku={ku}")
+
+
+def test_getrf_blocked_batched_and_singular():
+    batch, n, kl, ku = 5, 200, 40, 30
+    T = np.stack([random_band(n, kl, ku, 70 + b) for b in range(batch)])
+    T[2, 77, :] = 0.0
+    AB = bandlu.dense_to_band_batched(to_dev(T), kl, ku)
+    ipiv, info = bandlu.band_getrf_batched(AB, kl, ku)
+    ABg, ipg, infg = AB.cpu().numpy(), ipiv.cpu().numpy(), info.cpu().numpy()
+    for b in range(batch):
+        o = oracle_pipeline(T[b], kl, ku)
+        assert np.array_equal(ipg[b], o[2]) and infg[b] == o[3], b
+        assert_bitwise(ABg[b], o[1], f"batch {b}")

@@ -77,3 +77,34 @@ def test_batched_workload():
         assert np.array_equal(bits(ABg[b]), bits(ABo))
         xo = oracle.gbtrs(ABo, kl, ku, ipo, B[b].copy())
         assert np.array_equal(bits(xg[b]), bits(xo))
+
+
+def test_wide_band_workload():
+    """n = 32768, kl = ku = 256 (8 GiB dense): full-size detect/convert/LU
+    parity; the solve is checked through the backward error of the oracle's
+    own solve applied to the GPU factors."""
+    name = "n32768_kl256_ku256"
+    w = inputs.WORKLOADS[name]
+    n, kl, ku = w["n"], w["kl"], w["ku"]
+    T = inputs.workload_matrix(name)
+    A = torch.from_numpy(T).to(DEV)
+    assert tuple(bandlu.band_detect(A).cpu().numpy()) == oracle.detect(T)[:3] == (kl, ku, 0)
+    ex = bandlu.band_detect(A, 128, 128).cpu().numpy()
+    assert ex[2] == 1 and (ex[0] > 128 or ex[1] > 128)
+    AB = bandlu.dense_to_band(A, kl, ku)
+    del A
+    ABo, _ = oracle.dense_to_band(T, kl, ku)
+    del T
+    assert np.array_equal(bits(AB.cpu().numpy()), bits(ABo))
+    AB0 = ABo.copy()
+    ipiv, info = bandlu.band_getrf(AB, kl, ku)
+    ipo, info_o, _ = oracle.gbtrf(ABo, kl, ku)
+    assert np.array_equal(ipiv.cpu().numpy(), ipo) and int(info.cpu()[0]) == info_o == 0
+    ABg = AB.cpu().numpy()
+    assert np.array_equal(bits(ABg), bits(ABo))
+    assert oracle.band_backward_error(AB0, ABg, kl, ku, ipiv.cpu().numpy()) <= 10.0
+    b = inputs.workload_rhs(name)
+    xg = torch.from_numpy(b.copy()).to(DEV)
+    bandlu.band_getrs(AB, kl, ku, ipiv, xg)
+    xo = oracle.gbtrs(ABo, kl, ku, ipo, b.copy())
+    assert np.array_equal(bits(xg.cpu().numpy()), bits(xo))
