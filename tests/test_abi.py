@@ -74,10 +74,12 @@ def test_argument_validation(lib):
 
 
 def test_variant_selection(lib):
-    W, G16, GEN = 1, 2, 3
+    W, G16, GEN, BLK = 1, 2, 3, 4
     assert lib.band_getrf_variant(1000, 3, 3, 1) == W
     assert lib.band_getrf_variant(8192, 16, 16, 1) == W
     assert lib.band_getrf_variant(16384, 2, 64, 1) == W
     assert lib.band_getrf_variant(256, 4, 4, 4096) == G16
-    assert lib.band_getrf_variant(300, 40, 3, 1) == GEN
+    assert lib.band_getrf_variant(300, 40, 3, 1) == BLK
+    assert lib.band_getrf_variant(32768, 256, 256, 1) == BLK
+    assert lib.band_getrf_variant(2000, 300, 10, 1) == GEN
     assert lib.band_getrf_variant(-1, 0, 0, 1) == -1
