@@ -15,6 +15,7 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -42,6 +43,70 @@ def kernel_costs(n, kl, ku, batch):
                   "flops": 2.0 * n * kl * (kl + ku + 1) * batch},
         "getrs": {"bytes": (8.0 * ldab * n + 4.0 * n + 16.0 * n) * batch},
     }
+
+
+# HIP sources each step's kernels are built from
+STEP_SOURCES = {
+    "detect": ["detect.hip", "common.hpp"],
+    "convert": ["convert.hip", "common.hpp"],
+    "getrf": ["getrf.hip", "getrf_win64.hpp", "getrf_window.hpp", "getrf_blocked.hip", "bufio.hpp",
+              "common.hpp"],
+    "getrs": ["getrs.hip", "bufio.hpp", "common.hpp"],
+}
+
+
+def source_hash(step):
+    """sha256 over the sources of one step: its counters are valid only for these."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_22099_amd", "csrc")
+    files = list(STEP_SOURCES[step])
+    if step == "getrf":
+        files += sorted(f for f in os.listdir(csrc) if f.startswith("getrf_win_g"))
+    for f in files:
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` on `workload` from the committed
+    rocprofv3 counter summary (FETCH_SIZE + WRITE_SIZE, each scaled by the
+    same counter on a plain copy of known size), or None when there is no
+    summary or the kernels changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"counters_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("- ") and ":" in line:
+                k, v = line[2:].split(":", 1)
+                vals[k.strip()] = v.strip().strip("`")
+    if vals.get(f"{kernel}.source_sha256") != source_hash(kernel):
+        return None
+    try:
+        fetch = float(vals[f"{kernel}.FETCH_SIZE_KiB"])
+        write = float(vals[f"{kernel}.WRITE_SIZE_KiB"])
+        copy_bytes = float(vals["copy.bytes"])
+        fscale = copy_bytes / (float(vals["copy.FETCH_SIZE_KiB"]) * 1024.0)
+        wscale = copy_bytes / (float(vals["copy.WRITE_SIZE_KiB"]) * 1024.0)
+    except (KeyError, ValueError, ZeroDivisionError):
+        return None
+    return fetch * 1024.0 * fscale + write * 1024.0 * wscale
+
+
+def copy_calibration():
+    """A plain device copy of known size, profiled beside the path to scale
+    FETCH_SIZE / WRITE_SIZE into bytes."""
+    import torch
+
+    n = 64 * 1024 * 1024  # 512 MiB of doubles
+    a = torch.ones(n, dtype=torch.float64, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_per_launch": n * 8, "launches": 3}))
 
 
 def roofline_entry(name, t_ms, cost):
@@ -105,7 +170,12 @@ def main():
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense LU comparator")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 512 MiB device copy (counter calibration)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU only; the path is a single-GPU "
                                    "kernel pipeline (see DESIGN.md for how it would shard)",
@@ -215,6 +285,12 @@ def main():
         roof = {"bound": "hbm", "achieved": d["gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": d["frac_hbm"], "traffic": None}
     roof["kernel"] = dom
+    tb = measured_traffic(dom, args.workload)
+    roof["traffic"] = tb
+    for k in names:
+        t = measured_traffic(k, args.workload)
+        kernels[k]["traffic_bytes"] = t
+        kernels[k]["algorithmic_bytes"] = costs[k]["bytes"]
 
     out = {
         "metric": METRIC, "value": value, "unit": "factorizations/s", "n_gpus": 1,
