@@ -124,10 +124,13 @@ int dense_to_band_batched(const double *dA, int64_t n, int64_t lda, int64_t stri
  *   - *d_info (int32) = 0, or j+1 for the first exactly-zero pivot in 0-based
  *     column j; the factorisation still completes, as in xGBTRF.
  * Multipliers are formed as a * (1/pivot) when |pivot| >= DBL_MIN, else as
- * a / pivot; every update is one fused multiply-add.  For kl + ku below the
- * dense-contraction threshold the factors are bitwise those of the unblocked
- * algorithm; above it, a blocked variant with fp64 matrix-core updates is
- * used, whose pivots are identical and whose factors agree to rounding.
+ * a / pivot; every update is one fused multiply-add.  Below the
+ * dense-contraction threshold (kl < 32) the factors are bitwise those of the
+ * unblocked algorithm on finite data; from kl = 32 on (and kl <= 256) the
+ * blocked variant applies each panel of 32 columns to the rest of the band
+ * as a dense product on the fp64 matrix cores, which sums in another order:
+ * its factors agree with the unblocked ones to rounding, and so do its
+ * pivots unless two candidates of a column lie within rounding of each other.
  */
 int band_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab, int32_t *d_ipiv,
                int32_t *d_info, void *stream);
@@ -169,11 +172,25 @@ int band_getrs_batched(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const do
  * for these sizes (host-only, enqueues nothing).  Returns one of the
  * BANDLU_GETRF_* codes below, or a negative status for invalid sizes.
  */
-#define BANDLU_GETRF_WINDOW 1     /* register window, 64 lanes per matrix   */
-#define BANDLU_GETRF_WINDOW_G16 2 /* register window, 16 lanes per matrix   */
-#define BANDLU_GETRF_GENERIC 3    /* unblocked, one workgroup per matrix    */
-#define BANDLU_GETRF_BLOCKED 4    /* blocked, fp64 MFMA trailing update     */
+#define BANDLU_GETRF_WINDOW 1       /* register window, 64 lanes per matrix     */
+#define BANDLU_GETRF_WINDOW_G16 2   /* register window, 16 lanes per matrix     */
+#define BANDLU_GETRF_GENERIC 3      /* unblocked, one workgroup per matrix      */
+#define BANDLU_GETRF_BLOCKED 4      /* blocked, exact rank-1 trailing updates   */
+#define BANDLU_GETRF_BLOCKED_MFMA 5 /* blocked, fp64 MFMA trailing update       */
 int band_getrf_variant(int64_t n, int64_t kl, int64_t ku, int64_t batch);
+
+/*
+ * band_getrf_ex -- band_getrf_batched with the kernel chosen by the caller:
+ * variant 0 picks it as band_getrf_batched does, 1..5 forces that
+ * BANDLU_GETRF_* kernel.  Arguments 1-10 as in band_getrf_batched (argument
+ * 11 is the variant).  A variant that cannot handle the sizes (a window for
+ * kl > 31 or a band wider than its registers, a blocked variant for
+ * kl > 256) returns BANDLU_ERR_UNSUPPORTED and enqueues nothing.  For tests
+ * and measurements that compare the kernels on one input.
+ */
+int band_getrf_ex(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab, int64_t strideAB,
+                  int32_t *d_ipiv, int64_t strideP, int32_t *d_info, int64_t batch, int variant,
+                  void *stream);
 
 /* Text for a status code (static storage). */
 const char *band_status_string(int status);

@@ -47,6 +47,7 @@ EXPORTS = {
     "band_getrs_batched": [_i64, _i64, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _vp, _i64, _i64,
                            _i64, _vp],
     "band_getrf_variant": [_i64, _i64, _i64, _i64],
+    "band_getrf_ex": [_i64, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _vp, _i64, ctypes.c_int, _vp],
     "band_status_string": [ctypes.c_int],
     "band_last_error": [],
 }
@@ -56,7 +57,8 @@ for _name, _args in EXPORTS.items():
     _f.restype = ctypes.c_char_p if _name in ("band_status_string", "band_last_error") \
         else ctypes.c_int
 
-VARIANTS = {1: "window", 2: "window_g16", 3: "generic", 4: "blocked"}
+VARIANTS = {1: "window", 2: "window_g16", 3: "generic", 4: "blocked", 5: "blocked_mfma"}
+_VARIANT_CODES = {name: code for code, name in VARIANTS.items()}
 
 
 class BandLUError(RuntimeError):
@@ -154,19 +156,33 @@ def dense_to_band_batched(A, kl, ku, AB=None, ldab=None):
 
 
 # ------------------------------------------------------------------- getrf --
-def band_getrf(AB, kl, ku, ipiv=None, info=None):
-    """In-place band LU; returns (ipiv int32 (n,), info int32 (1,)) on device."""
+def _variant_code(variant):
+    if variant is None:
+        return 0
+    if variant not in _VARIANT_CODES:
+        raise ValueError(f"unknown variant {variant!r}; one of {sorted(_VARIANT_CODES)}")
+    return _VARIANT_CODES[variant]
+
+
+def band_getrf(AB, kl, ku, ipiv=None, info=None, variant=None):
+    """In-place band LU; returns (ipiv int32 (n,), info int32 (1,)) on device.
+    ``variant`` (a name from VARIANTS) forces a kernel through band_getrf_ex."""
     _check(AB, torch.float64, "AB", 2)
     n = AB.shape[0]
     if ipiv is None:
         ipiv = torch.empty(n, dtype=torch.int32, device=AB.device)
     if info is None:
         info = torch.empty(1, dtype=torch.int32, device=AB.device)
-    _call("band_getrf", n, kl, ku, _ptr(AB), max(_ld(AB), 1), _ptr(ipiv), _ptr(info), _stream())
+    ldab = max(_ld(AB), 1)
+    if variant is None:
+        _call("band_getrf", n, kl, ku, _ptr(AB), ldab, _ptr(ipiv), _ptr(info), _stream())
+    else:
+        _call("band_getrf_ex", n, kl, ku, _ptr(AB), ldab, ldab * n, _ptr(ipiv), n, _ptr(info), 1,
+              _variant_code(variant), _stream())
     return ipiv, info
 
 
-def band_getrf_batched(AB, kl, ku, ipiv=None, info=None):
+def band_getrf_batched(AB, kl, ku, ipiv=None, info=None, variant=None):
     """In-place batched band LU; returns (ipiv (batch, n), info (batch,))."""
     _check(AB, torch.float64, "AB", 3)
     batch, n = AB.shape[0], AB.shape[1]
@@ -177,8 +193,12 @@ def band_getrf_batched(AB, kl, ku, ipiv=None, info=None):
     ldab = max(_ld(AB), 1)
     sAB = AB.stride(0) if batch > 1 else ldab * n
     sP = ipiv.stride(0) if batch > 1 else n
-    _call("band_getrf_batched", n, kl, ku, _ptr(AB), ldab, sAB, _ptr(ipiv), sP, _ptr(info), batch,
-          _stream())
+    if variant is None:
+        _call("band_getrf_batched", n, kl, ku, _ptr(AB), ldab, sAB, _ptr(ipiv), sP, _ptr(info),
+              batch, _stream())
+    else:
+        _call("band_getrf_ex", n, kl, ku, _ptr(AB), ldab, sAB, _ptr(ipiv), sP, _ptr(info), batch,
+              _variant_code(variant), _stream())
     return ipiv, info
 
 

@@ -6,13 +6,16 @@
 //               register window, 64 lanes per matrix (getrf_win64.hpp);
 //   WINDOW_G16  batched, kl <= 7 and 2kl+ku+1 <= 32: register window, 16
 //               lanes per matrix, four matrices per wavefront;
-//   BLOCKED     everything else with kl <= 256: panels of 32 columns factored
-//               in LDS, trailing band updated by many workgroups
-//               (getrf_blocked.hip);
+//   BLOCKED     kl <= 31 beyond the windows: panels of 32 columns factored in
+//               registers, trailing band updated by many workgroups with the
+//               unblocked rank-1 order (getrf_blocked.hip);
+//   BLOCKED_MFMA  32 <= kl <= 256: the same panels, trailing band updated as
+//               a dense product on the fp64 matrix cores (getrf_mfma.hip);
 //   GENERIC     kl > 256: one workgroup per matrix works on the band in global
 //               memory, one column step at a time.
-// The window, blocked-exact and generic kernels produce bitwise the factors of
-// the unblocked algorithm on finite data.
+// The window, blocked and generic kernels produce bitwise the factors of the
+// unblocked algorithm on finite data; the matrix-core variant agrees to
+// rounding.  band_getrf_ex runs a named variant.
 #include <cfloat>
 #include <climits>
 
@@ -48,7 +51,10 @@ WinKernel win_kernel(int G, int CPL, int H) {
 
 int launch_getrf_blocked(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
                          int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info,
-                         int64_t batch, bool use_mfma, hipStream_t s);
+                         int64_t batch, hipStream_t s);
+int launch_getrf_mfma(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
+                      int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info,
+                      int64_t batch, hipStream_t s);
 
 namespace {
 
@@ -165,17 +171,40 @@ __global__ void zero_info_kernel(int32_t *info, int64_t batch) {
 
 int select_variant(int64_t n, int64_t kl, int64_t ku, int64_t batch) {
     const int64_t need = 2 * kl + ku + 1;
-    (void)n;
     if (batch >= 64 && kl <= 7 && need <= 32) return BANDLU_GETRF_WINDOW_G16;
     if (kl <= 31 && (need <= 64 || (need <= 128 && kl <= 15)) && need * n * 8 <= kMaxBufferBytes)
         return BANDLU_GETRF_WINDOW;
-    if (kl <= 256 && n <= INT32_MAX && batch <= 65535) return BANDLU_GETRF_BLOCKED;
+    // from kl = 32 on, applying a panel of 32 columns is a real dense product
+    // (at least 32 x 32 x 32): matrix cores
+    if (kl <= 256 && n <= INT32_MAX && batch <= 65535)
+        return kl >= 32 ? BANDLU_GETRF_BLOCKED_MFMA : BANDLU_GETRF_BLOCKED;
     return BANDLU_GETRF_GENERIC;
+}
+
+// Whether a variant can factor these sizes (the window kernels address the
+// band through a range-checked buffer of at most 2 GiB and keep the window in
+// registers; the blocked kernels hold a panel of NB + kl rows in one workgroup).
+bool variant_fits(int v, int64_t n, int64_t kl, int64_t ku, int64_t ldab, int64_t batch) {
+    const int64_t need = 2 * kl + ku + 1;
+    switch (v) {
+    case BANDLU_GETRF_WINDOW_G16:
+        return kl <= 7 && need <= 32 && ldab * n * 8 <= kMaxBufferBytes;
+    case BANDLU_GETRF_WINDOW:
+        return kl <= 31 && (need <= 64 || (need <= 128 && kl <= 15)) &&
+               ldab * n * 8 <= kMaxBufferBytes;
+    case BANDLU_GETRF_BLOCKED:
+    case BANDLU_GETRF_BLOCKED_MFMA:
+        return kl <= 256 && batch <= 65535;
+    case BANDLU_GETRF_GENERIC:
+        return true;
+    default:
+        return false;
+    }
 }
 
 int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
                  int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info,
-                 int64_t batch, hipStream_t s) {
+                 int64_t batch, int variant, hipStream_t s) {
     if (batch == 0) return BANDLU_OK;
     if (n == 0) {
         hipLaunchKernelGGL(zero_info_kernel, dim3((unsigned)((batch + 255) / 256)), dim3(256), 0,
@@ -183,11 +212,16 @@ int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
         BANDLU_CHECK_LAUNCH("band_getrf (n = 0)");
         return BANDLU_OK;
     }
-    int v = select_variant(n, kl, ku, batch);
     const int64_t need = 2 * kl + ku + 1;
-    // the single-matrix window kernel addresses the band through a range-checked
-    // buffer of at most 2 GiB
-    if (v == BANDLU_GETRF_WINDOW && ldab * n * 8 > kMaxBufferBytes) v = BANDLU_GETRF_GENERIC;
+    int v = variant;
+    if (v == 0) {
+        v = select_variant(n, kl, ku, batch);
+        if (!variant_fits(v, n, kl, ku, ldab, batch)) v = BANDLU_GETRF_GENERIC;
+    } else if (!variant_fits(v, n, kl, ku, ldab, batch)) {
+        set_error("band_getrf: variant %d cannot factor n = %lld, kl = %lld, ku = %lld", v,
+                  (long long)n, (long long)kl, (long long)ku);
+        return BANDLU_ERR_UNSUPPORTED;
+    }
     if (v == BANDLU_GETRF_WINDOW || v == BANDLU_GETRF_WINDOW_G16) {
         WinParams W;
         W.AB = dAB;
@@ -220,7 +254,9 @@ int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
     }
     if (v == BANDLU_GETRF_BLOCKED)
         return launch_getrf_blocked(n, kl, ku, dAB, ldab, strideAB, d_ipiv, strideP, d_info, batch,
-                                    false, s);
+                                    s);
+    if (v == BANDLU_GETRF_BLOCKED_MFMA)
+        return launch_getrf_mfma(n, kl, ku, dAB, ldab, strideAB, d_ipiv, strideP, d_info, batch, s);
     GenParams P;
     P.AB = dAB;
     P.ipiv = d_ipiv;
@@ -265,7 +301,7 @@ extern "C" int band_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_
         set_error("band_getrf: n >= 2^31 is not supported");
         return BANDLU_ERR_UNSUPPORTED;
     }
-    return launch_getrf(n, kl, ku, dAB, ldab, ldab * n, d_ipiv, n, d_info, 1, as_stream(stream));
+    return launch_getrf(n, kl, ku, dAB, ldab, ldab * n, d_ipiv, n, d_info, 1, 0, as_stream(stream));
 }
 
 extern "C" int band_getrf_batched(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
@@ -287,6 +323,31 @@ extern "C" int band_getrf_batched(int64_t n, int64_t kl, int64_t ku, double *dAB
         set_error("band_getrf_batched: sizes too large");
         return BANDLU_ERR_UNSUPPORTED;
     }
-    return launch_getrf(n, kl, ku, dAB, ldab, strideAB, d_ipiv, strideP, d_info, batch,
+    return launch_getrf(n, kl, ku, dAB, ldab, strideAB, d_ipiv, strideP, d_info, batch, 0,
+                        as_stream(stream));
+}
+
+extern "C" int band_getrf_ex(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
+                             int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info,
+                             int64_t batch, int variant, void *stream) {
+    clear_error();
+    const int64_t bmax = n > 1 ? n - 1 : 0;
+    BANDLU_ARG(n >= 0, 1, "band_getrf_ex: n < 0");
+    BANDLU_ARG(kl >= 0 && kl <= bmax, 2, "band_getrf_ex: kl out of range");
+    BANDLU_ARG(ku >= 0 && ku <= bmax, 3, "band_getrf_ex: ku out of range");
+    BANDLU_ARG(n == 0 || batch == 0 || dAB != nullptr, 4, "band_getrf_ex: dAB is null");
+    BANDLU_ARG(ldab >= 2 * kl + ku + 1, 5, "band_getrf_ex: ldab < 2kl+ku+1");
+    BANDLU_ARG(batch <= 1 || strideAB >= ldab * n, 6, "band_getrf_ex: strideAB < ldab*n");
+    BANDLU_ARG(n == 0 || batch == 0 || d_ipiv != nullptr, 7, "band_getrf_ex: d_ipiv is null");
+    BANDLU_ARG(batch <= 1 || strideP >= n, 8, "band_getrf_ex: strideP < n");
+    BANDLU_ARG(batch == 0 || d_info != nullptr, 9, "band_getrf_ex: d_info is null");
+    BANDLU_ARG(batch >= 0, 10, "band_getrf_ex: batch < 0");
+    BANDLU_ARG(variant >= 0 && variant <= BANDLU_GETRF_BLOCKED_MFMA, 11,
+               "band_getrf_ex: unknown variant");
+    if (n > kMaxN || batch > INT_MAX) {
+        set_error("band_getrf_ex: sizes too large");
+        return BANDLU_ERR_UNSUPPORTED;
+    }
+    return launch_getrf(n, kl, ku, dAB, ldab, strideAB, d_ipiv, strideP, d_info, batch, variant,
                         as_stream(stream));
 }

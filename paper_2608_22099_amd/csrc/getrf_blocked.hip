@@ -21,12 +21,15 @@
 
 #include "bufio.hpp"
 #include "common.hpp"
+#include "wave.hpp"
 
 namespace bandlu {
 
 int launch_getrf_blocked(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
                          int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info,
-                         int64_t batch, bool use_mfma, hipStream_t s);
+                         int64_t batch, hipStream_t s);
+int launch_band_zero_fill(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
+                          int64_t strideAB, int32_t *d_info, int64_t batch, hipStream_t s);
 
 namespace {
 
@@ -34,13 +37,6 @@ constexpr int NB = 32;        // panel width
 constexpr int NBC = 32;       // trailing block width
 constexpr int kMaxKl = 256;   // one thread per row: NB + NB + kl <= 320 threads
 
-struct BlkParams {
-    double *AB;
-    int32_t *ipiv;
-    int32_t *info;
-    int64_t ldab, strideAB, strideP;
-    int n, kl, ku, j0, nb;
-};
 
 // ------------------------------------------------------------- fused step --
 // One launch per panel.  Workgroup x of the launch owns the 32 columns
@@ -64,18 +60,6 @@ struct StepParams {
     int jn;          // first column of the blocks (= next panel when has_factor)
     int has_update, has_factor;
 };
-
-#define DPP_D(v, ctrl)                                                                         \
-    __longlong_as_double(                                                                      \
-        ((long long)__builtin_amdgcn_mov_dpp((int)(__double_as_longlong(v) >> 32), ctrl, 0xf,  \
-                                             0xf, false)                                       \
-         << 32) |                                                                              \
-        (unsigned)__builtin_amdgcn_mov_dpp((int)(__double_as_longlong(v) & 0xffffffffll), ctrl, \
-                                           0xf, 0xf, false))
-
-__device__ __forceinline__ bool kbetter(double ka, int ia, double kb, int ib) {
-    return ka > kb || (ka == kb && ia < ib);
-}
 
 __global__ __launch_bounds__(kRows) void blk_step_kernel(StepParams P) {
     const int bmat = blockIdx.y;
@@ -108,29 +92,34 @@ __global__ __launch_bounds__(kRows) void blk_step_kernel(StepParams P) {
     __shared__ int s_piv[NB];
 
     double x[NBC];
+    unsigned okx = 0;
 #pragma unroll
     for (int c = 0; c < NBC; ++c) {
         const int col = cb + c;
-        const bool ok = own && c < W && col - r <= kv && r - col <= kl;
-        x[c] = ok ? AB[int64_t(col) * ldab + (kv + r - col)] : 0.0;
+        const bool ok = own & (c < W) & (col - r <= kv) & (r - col <= kl);
+        okx |= unsigned(ok) << c;
+        x[c] = ld_clamped(AB, int64_t(col) * ldab + (kv + r - col), ok);
     }
+#pragma unroll
+    for (int c = 0; c < NBC; ++c) x[c] = keep_if(x[c], okx, c);
     int step = 0;  // parity of the LDS row buffers
 
     // ---------------------------------------------------------- phase A --
     if (upd) {
         // the panel's pivots, staged once
         if (t < nb) s_piv[t] = ipiv[j0 + t] - 1 - (j0 + t);
-        // multiplier of panel column jj for this thread's row, loaded 4 steps ahead
+        // multiplier of panel column jj for this thread's row, loaded 4 steps
+        // ahead (only used by rows that have one: no need to clear the others)
         auto lval = [&](int jj) -> double {
             const int j = j0 + jj;
             const int tt = t - jj;
-            const bool ok = own && jj < nb && tt >= 1 && tt <= min(kl, n - 1 - j);
-            return ok ? AB[int64_t(j) * ldab + (kv + tt)] : 0.0;
+            const bool ok = own & (jj < nb) & (tt >= 1) & (tt <= min(kl, n - 1 - j));
+            return ld_clamped(AB, int64_t(j) * ldab + (kv + tt), ok);
         };
         double lr[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) lr[q] = lval(q);
-        __syncthreads();
+        lds_barrier();
 #pragma unroll 1
         for (int j4 = 0; j4 < nb; j4 += 4) {
 #pragma unroll
@@ -152,7 +141,7 @@ __global__ __launch_bounds__(kRows) void blk_step_kernel(StepParams P) {
 #pragma unroll
                         for (int c = 0; c < NBC; ++c) T2[A][c] = x[c];
                     }
-                    __syncthreads();
+                    lds_barrier();
                     if (t == jj) {
 #pragma unroll
                         for (int c = 0; c < NBC; ++c) x[c] = S[A][c];
@@ -185,10 +174,10 @@ __global__ __launch_bounds__(kRows) void blk_step_kernel(StepParams P) {
                 // wave max by DPP inside rows of 16 lanes, then across the 4 rows;
                 // rows are in lane order, so the lowest matching lane is the first index
                 double km16 = key;
-                km16 = fmax(km16, DPP_D(km16, 0xB1));   // quad_perm [1,0,3,2]
-                km16 = fmax(km16, DPP_D(km16, 0x4E));   // quad_perm [2,3,0,1]
-                km16 = fmax(km16, DPP_D(km16, 0x141));  // row_half_mirror
-                km16 = fmax(km16, DPP_D(km16, 0x140));  // row_mirror
+                km16 = fmax(km16, dpp_d<0xB1>(km16));   // quad_perm [1,0,3,2]
+                km16 = fmax(km16, dpp_d<0x4E>(km16));   // quad_perm [2,3,0,1]
+                km16 = fmax(km16, dpp_d<0x141>(km16));  // row_half_mirror
+                km16 = fmax(km16, dpp_d<0x140>(km16));  // row_mirror
                 const double wmax = fmax(fmax(readlane_d(km16, 0), readlane_d(km16, 16)),
                                          fmax(readlane_d(km16, 32), readlane_d(km16, 48)));
                 const unsigned long long hit = __ballot(key == wmax);
@@ -198,12 +187,12 @@ __global__ __launch_bounds__(kRows) void blk_step_kernel(StepParams P) {
                     s_idx[wv] = wv * 64 + first - off - jj;
                     s_val[wv] = readlane_d(v, first);
                 }
-                __syncthreads();
+                lds_barrier();
                 double bk = s_key[0], bv = s_val[0];
                 int bi = s_idx[0];
 #pragma unroll
                 for (int w = 1; w < kRows / 64; ++w)
-                    if (kbetter(s_key[w], s_idx[w], bk, bi)) { bk = s_key[w]; bi = s_idx[w]; bv = s_val[w]; }
+                    if (key_better(s_key[w], s_idx[w], bk, bi)) { bk = s_key[w]; bi = s_idx[w]; bv = s_val[w]; }
                 const int p = bi;
                 if (t == 0) ipiv[j] = j + p + 1;
                 const int A = step & 1;
@@ -217,7 +206,7 @@ __global__ __launch_bounds__(kRows) void blk_step_kernel(StepParams P) {
 #pragma unroll
                         for (int c = 0; c < NBC; ++c) T2[A][c] = x[c];
                     }
-                    __syncthreads();
+                    lds_barrier();
                     // the interchange covers panel columns jj..; earlier columns
                     // keep their multipliers (product form of L)
                     if (t == off + jj) {
@@ -237,7 +226,7 @@ __global__ __launch_bounds__(kRows) void blk_step_kernel(StepParams P) {
                     }
                 } else {
                     if (info == 0) info = j + 1;
-                    __syncthreads();  // keep one barrier per step on every path
+                    lds_barrier();  // keep one barrier per step on every path
                 }
             }
         }
@@ -251,48 +240,42 @@ __global__ __launch_bounds__(kRows) void blk_step_kernel(StepParams P) {
     }
 }
 
-__global__ void zero_fill_kernel(BlkParams P, int64_t batch) {
+__global__ void zero_fill_kernel(double *ABbase, int64_t ldab, int64_t strideAB, int32_t *info,
+                                 int n, int kl, int ku, int64_t batch) {
     // in-matrix fill slots (band rows 0..kl-1) start at zero; info starts at 0
-    const int n = P.n, kl = P.kl, kv = P.kl + P.ku;
+    const int kv = kl + ku;
     const int64_t total = int64_t(n) * kl;
     for (int64_t b = blockIdx.y; b < batch; b += gridDim.y) {
-        double *AB = P.AB + b * P.strideAB;
+        double *AB = ABbase + b * strideAB;
         for (int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; e < total;
              e += int64_t(gridDim.x) * blockDim.x) {
             const int64_t c = e / kl, r = e - c * kl;
-            if (r >= kv - c) AB[c * P.ldab + r] = 0.0;
+            if (r >= kv - c) AB[c * ldab + r] = 0.0;
         }
-        if (blockIdx.x == 0 && threadIdx.x == 0) P.info[b] = 0;
+        if (blockIdx.x == 0 && threadIdx.x == 0) info[b] = 0;
     }
 }
 
 }  // namespace
 
+int launch_band_zero_fill(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
+                          int64_t strideAB, int32_t *d_info, int64_t batch, hipStream_t s) {
+    const int64_t total = n * kl;
+    const unsigned gx = (unsigned)std::max<int64_t>(1, std::min<int64_t>((total + 255) / 256, 4096));
+    hipLaunchKernelGGL(zero_fill_kernel, dim3(gx, (unsigned)std::min<int64_t>(batch, 65535)),
+                       dim3(256), 0, s, dAB, ldab, strideAB, d_info, (int)n, (int)kl, (int)ku, batch);
+    BANDLU_CHECK_LAUNCH("band_getrf (fill-row init)");
+    return BANDLU_OK;
+}
+
 int launch_getrf_blocked(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
                          int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info,
-                         int64_t batch, bool use_mfma, hipStream_t s) {
-    (void)use_mfma;
+                         int64_t batch, hipStream_t s) {
     if (kl > kMaxKl || batch > 65535) {
         set_error("band_getrf: blocked variant needs kl <= %d", kMaxKl);
         return BANDLU_ERR_UNSUPPORTED;
     }
-    BlkParams P;
-    P.AB = dAB;
-    P.ipiv = d_ipiv;
-    P.info = d_info;
-    P.ldab = ldab;
-    P.strideAB = strideAB;
-    P.strideP = strideP;
-    P.n = (int)n;
-    P.kl = (int)kl;
-    P.ku = (int)ku;
-    {
-        const int64_t total = n * kl;
-        const unsigned gx = (unsigned)std::max<int64_t>(1, std::min<int64_t>((total + 255) / 256, 4096));
-        hipLaunchKernelGGL(zero_fill_kernel, dim3(gx, (unsigned)std::min<int64_t>(batch, 65535)),
-                           dim3(256), 0, s, P, batch);
-        BANDLU_CHECK_LAUNCH("band_getrf (blocked init)");
-    }
+    if (int rc = launch_band_zero_fill(n, kl, ku, dAB, ldab, strideAB, d_info, batch, s)) return rc;
     const int kv = int(kl + ku);
     StepParams Q;
     Q.AB = dAB;

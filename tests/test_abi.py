@@ -32,6 +32,7 @@ def lib():
     L.band_getrf_batched.argtypes = [i64, i64, i64, vp, i64, i64, vp, i64, vp, i64, vp]
     L.band_getrs.argtypes = [i64, i64, i64, i64, vp, i64, vp, vp, i64, vp]
     L.band_getrf_variant.argtypes = [i64, i64, i64, i64]
+    L.band_getrf_ex.argtypes = [i64, i64, i64, vp, i64, i64, vp, i64, vp, i64, ctypes.c_int, vp]
     L.band_status_string.restype = ctypes.c_char_p
     L.band_last_error.restype = ctypes.c_char_p
     return L
@@ -41,7 +42,7 @@ def test_header_declares_the_path():
     names = declared_functions()
     for f in ["band_detect", "band_detect_batched", "dense_to_band", "dense_to_band_batched",
               "band_getrf", "band_getrf_batched", "band_getrs", "band_getrs_batched",
-              "band_status_string", "band_last_error", "band_getrf_variant"]:
+              "band_status_string", "band_last_error", "band_getrf_variant", "band_getrf_ex"]:
         assert f in names
 
 
@@ -69,17 +70,28 @@ def test_argument_validation(lib):
     assert lib.band_getrf_batched(10, 2, 3, fake, 8, 80, fake, 9, fake, 2, None) == -8
     assert lib.band_getrs(10, 2, 3, -1, fake, 8, fake, fake, 10, None) == -4
     assert lib.band_getrs(10, 2, 3, 1, fake, 8, fake, fake, 9, None) == -9
+    # band_getrf_ex: argument 11 is the variant; a variant that cannot take the
+    # sizes is refused before anything is enqueued
+    assert lib.band_getrf_ex(10, 2, 3, fake, 8, 80, fake, 10, fake, 1, 6, None) == -11
+    assert lib.band_getrf_ex(10, 2, 3, fake, 8, 80, fake, 10, fake, 1, -1, None) == -11
+    assert lib.band_getrf_ex(100, 40, 3, fake, 84, 8400, fake, 100, fake, 1, 1, None) == -1001
+    assert b"variant 1" in lib.band_last_error()
+    assert lib.band_getrf_ex(600, 300, 3, fake, 604, 0, fake, 600, fake, 1, 5, None) == -1001
+    assert lib.band_getrf_ex(600, 300, 3, fake, 604, 0, fake, 600, fake, 1, 4, None) == -1001
     assert lib.band_status_string(-3) == b"invalid argument"
     assert lib.band_status_string(-1000).startswith(b"HIP")
 
 
 def test_variant_selection(lib):
-    W, G16, GEN, BLK = 1, 2, 3, 4
+    W, G16, GEN, BLK, MF = 1, 2, 3, 4, 5
     assert lib.band_getrf_variant(1000, 3, 3, 1) == W
     assert lib.band_getrf_variant(8192, 16, 16, 1) == W
     assert lib.band_getrf_variant(16384, 2, 64, 1) == W
     assert lib.band_getrf_variant(256, 4, 4, 4096) == G16
-    assert lib.band_getrf_variant(300, 40, 3, 1) == BLK
-    assert lib.band_getrf_variant(32768, 256, 256, 1) == BLK
+    assert lib.band_getrf_variant(300, 40, 3, 1) == MF
+    assert lib.band_getrf_variant(32768, 256, 256, 1) == MF
+    assert lib.band_getrf_variant(300, 31, 90, 1) == BLK
+    assert lib.band_getrf_variant(300, 20, 100, 1) == BLK
+    assert lib.band_getrf_variant(300, 32, 0, 1) == MF
     assert lib.band_getrf_variant(2000, 300, 10, 1) == GEN
     assert lib.band_getrf_variant(-1, 0, 0, 1) == -1

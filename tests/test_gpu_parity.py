@@ -7,6 +7,7 @@ import numpy as np
 import pytest
 
 import oracle
+from checks import assert_backward_error, assert_factors_close
 from paper_2608_22099_amd import inputs
 
 pytestmark = pytest.mark.gpu
@@ -42,12 +43,12 @@ def assert_bitwise(g, o, what, nan_payload=False):
     assert bad[0].size == 0, f"{what}: {bad[0].size} mismatches, first at {tuple(b[0] for b in bad)}: gpu={g[tuple(b[0] for b in bad)]!r} oracle={o[tuple(b[0] for b in bad)]!r}"
 
 
-def gpu_pipeline(T, kl, ku, ldab=None):
+def gpu_pipeline(T, kl, ku, ldab=None, variant=None):
     """dense -> band -> getrf on the GPU; returns numpy (AB0, ABf, ipiv, info)."""
     A = to_dev(T)
     AB = bandlu.dense_to_band(A, kl, ku, ldab=ldab)
     AB0 = AB.cpu().numpy()
-    ipiv, info = bandlu.band_getrf(AB, kl, ku)
+    ipiv, info = bandlu.band_getrf(AB, kl, ku, variant=variant)
     torch.cuda.synchronize()
     return AB0, AB.cpu().numpy(), ipiv.cpu().numpy(), int(info.cpu()[0])
 
@@ -166,7 +167,12 @@ def test_getrf_random_shapes(seed):
     variant = bandlu.band_getrf_variant(n, kl, ku)
     assert np.array_equal(g[2], o[2]), f"ipiv ({variant})"
     assert g[3] == o[3]
-    assert_bitwise(g[1], o[1], f"factors ({variant}, n={n}, kl={kl}, ku={ku})")
+    what = f"factors ({variant}, n={n}, kl={kl}, ku={ku})"
+    if variant == "blocked_mfma":
+        assert_factors_close(g[1], o[1], kl, ku, what)
+        assert_backward_error(o[0], g[1], kl, ku, g[2], what)
+    else:
+        assert_bitwise(g[1], o[1], what)
 
 
 @pytest.mark.parametrize("kl,ku", [(0, 0), (1, 0), (0, 1), (3, 3), (16, 16), (2, 64), (31, 3),
@@ -306,12 +312,17 @@ def test_getrs_batched():
 
 
 # ----------------------------------------------------------- blocked getrf --
-@pytest.mark.parametrize("n,kl,ku", [(300, 40, 3), (95, 20, 52), (700, 100, 150), (1100, 256, 256),
-                                     (530, 33, 200), (64, 63, 63), (257, 32, 0), (400, 250, 1)])
+BLOCKED_SHAPES = [(300, 40, 3), (95, 20, 52), (700, 100, 150), (1100, 256, 256), (530, 33, 200),
+                  (64, 63, 63), (257, 32, 0), (400, 250, 1), (300, 31, 90), (97, 12, 80)]
+
+
+@pytest.mark.parametrize("n,kl,ku", BLOCKED_SHAPES)
 def test_getrf_blocked_exact(n, kl, ku):
-    assert bandlu.band_getrf_variant(n, kl, ku) == "blocked"
+    """The blocked kernel with rank-1 trailing updates is bitwise the unblocked
+    algorithm (forced through band_getrf_ex where the matrix-core variant
+    would be chosen)."""
     T = random_band(n, kl, ku, 31 * n + kl)
-    g, o = gpu_pipeline(T, kl, ku), oracle_pipeline(T, kl, ku)
+    g, o = gpu_pipeline(T, kl, ku, variant="blocked"), oracle_pipeline(T, kl, ku)
     assert np.array_equal(g[2], o[2]) and g[3] == o[3]
     assert_bitwise(g[1], o[1], f"blocked n={n} kl={kl} ku={ku}")
 
@@ -321,9 +332,89 @@ def test_getrf_blocked_batched_and_singular():
     T = np.stack([random_band(n, kl, ku, 70 + b) for b in range(batch)])
     T[2, 77, :] = 0.0
     AB = bandlu.dense_to_band_batched(to_dev(T), kl, ku)
-    ipiv, info = bandlu.band_getrf_batched(AB, kl, ku)
+    ipiv, info = bandlu.band_getrf_batched(AB, kl, ku, variant="blocked")
     ABg, ipg, infg = AB.cpu().numpy(), ipiv.cpu().numpy(), info.cpu().numpy()
     for b in range(batch):
         o = oracle_pipeline(T[b], kl, ku)
         assert np.array_equal(ipg[b], o[2]) and infg[b] == o[3], b
         assert_bitwise(ABg[b], o[1], f"batch {b}")
+
+
+# ------------------------------------------------------ matrix-core getrf --
+def check_mfma(T, kl, ku, what, variant=None):
+    g, o = gpu_pipeline(T, kl, ku, variant=variant), oracle_pipeline(T, kl, ku)
+    assert np.array_equal(g[2], o[2]), f"{what}: ipiv"
+    assert g[3] == o[3], f"{what}: info {g[3]} vs {o[3]}"
+    assert_factors_close(g[1], o[1], kl, ku, what)
+    if np.any(o[0] != 0.0):
+        assert_backward_error(o[0], g[1], kl, ku, g[2], what)
+    return g, o
+
+
+@pytest.mark.parametrize("n,kl,ku", [(300, 40, 3), (700, 100, 150), (1100, 256, 256), (530, 33, 200),
+                                     (64, 63, 63), (257, 32, 0), (400, 250, 1), (33, 32, 0),
+                                     (64, 32, 31), (65, 40, 24), (96, 50, 45), (289, 256, 32),
+                                     (600, 256, 343), (128, 127, 0)])
+def test_getrf_mfma_shapes(n, kl, ku):
+    """Panels of 32 with a ragged last panel, bands that reach one or many
+    column blocks, kl at both ends of the variant's range."""
+    assert bandlu.band_getrf_variant(n, kl, ku) == "blocked_mfma"
+    check_mfma(random_band(n, kl, ku, 7 * n + kl + ku), kl, ku, f"n={n} kl={kl} ku={ku}")
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_getrf_mfma_random(seed):
+    rng = np.random.default_rng(4000 + seed)
+    n = int(rng.integers(33, 900))
+    kl = int(rng.integers(32, min(n, 257)))
+    ku = int(rng.integers(0, min(n, 300)))
+    check_mfma(random_band(n, kl, ku, 600 + seed), kl, ku, f"seed {seed} n={n} kl={kl} ku={ku}")
+
+
+@pytest.mark.parametrize("n,kl,ku", [(40, 0, 0), (70, 3, 2), (100, 10, 5), (50, 20, 49),
+                                     (31, 5, 5), (1, 0, 0), (2, 1, 1)])
+def test_getrf_mfma_forced_narrow(n, kl, ku):
+    """The matrix-core kernel also factors narrow bands when forced (blocks
+    narrower than a panel, a band that does not reach the next panel)."""
+    check_mfma(random_band(n, kl, ku, 11 * n + kl), kl, ku, f"forced n={n} kl={kl} ku={ku}",
+               variant="blocked_mfma")
+
+
+def test_getrf_mfma_pivoting_and_singular():
+    """Heavy pivoting (rows scaled so the pivot is rarely the diagonal) and
+    exactly singular columns: info and ipiv match; a zero column leaves the
+    factorisation running."""
+    n, kl, ku = 300, 40, 20
+    T = random_band(n, kl, ku, 42)
+    T *= np.exp(np.random.default_rng(1).uniform(-3, 3, size=(1, n)))  # scales rows of A
+    check_mfma(T, kl, ku, "scaled rows")
+    for col in (0, 31, 32, 200, n - 1):
+        S = random_band(n, kl, ku, 43 + col)
+        S[col, :] = 0.0  # T[j, :] is column j of A
+        g, o = check_mfma(S, kl, ku, f"zero column {col}")
+        assert o[3] == col + 1
+    Z = np.zeros((70, 70))
+    g, o = check_mfma(Z, 33, 2, "zero matrix")
+    assert g[3] == 1
+
+
+def test_getrf_mfma_batched():
+    batch, n, kl, ku = 6, 230, 48, 40
+    T = np.stack([random_band(n, kl, ku, 300 + b) for b in range(batch)])
+    T[3, 100, :] = 0.0
+    AB = bandlu.dense_to_band_batched(to_dev(T), kl, ku)
+    AB0 = AB.cpu().numpy()
+    ipiv, info = bandlu.band_getrf_batched(AB, kl, ku)
+    ABg, ipg, infg = AB.cpu().numpy(), ipiv.cpu().numpy(), info.cpu().numpy()
+    for b in range(batch):
+        o = oracle_pipeline(T[b], kl, ku)
+        assert np.array_equal(ipg[b], o[2]) and infg[b] == o[3], b
+        assert_factors_close(ABg[b], o[1], kl, ku, f"batch {b}")
+        assert_backward_error(AB0[b], ABg[b], kl, ku, ipg[b], f"batch {b}")
+
+
+def test_getrf_mfma_deterministic():
+    T = random_band(700, 64, 64, 3)
+    a = gpu_pipeline(T, 64, 64)
+    b = gpu_pipeline(T, 64, 64)
+    assert_bitwise(a[1], b[1], "rerun")
