@@ -39,6 +39,17 @@ __device__ __forceinline__ void buf_st(Buf b, uint32_t byte_off, double v) {
         byte_off, 0, 0);
 }
 
+// The same with a wave-uniform part of the offset in a scalar register.
+__device__ __forceinline__ double buf_ld_so(Buf b, uint32_t voff, uint32_t soff) {
+    return __builtin_bit_cast(double, __builtin_amdgcn_raw_buffer_load_b64(b.r, voff, soff, 0));
+}
+
+__device__ __forceinline__ void buf_st_so(Buf b, uint32_t voff, uint32_t soff, double v) {
+    __builtin_amdgcn_raw_buffer_store_b64(
+        __builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(b.r, 0, 0, 0)), v), b.r,
+        voff, soff, 0);
+}
+
 __device__ __forceinline__ int buf_ld_i32(Buf b, uint32_t byte_off) {
     return (int)__builtin_amdgcn_raw_buffer_load_b32(b.r, byte_off, 0, 0);
 }

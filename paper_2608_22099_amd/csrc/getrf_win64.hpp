@@ -36,6 +36,7 @@
 #include "bufio.hpp"
 #include "common.hpp"
 #include "getrf_window.hpp"
+#include "getrf_win2.hpp"
 
 namespace bandlu {
 
@@ -292,12 +293,20 @@ __global__ __launch_bounds__(64) void getrf_win64_kernel(WinParams P) {
     if (L == 0) P.info[b] = info;
 }
 
+// One column per lane with a transposed pivot column from H = 7 on
+// (getrf_win2.hpp); the in-lane pivot scan below that and for two columns per
+// lane.
+template <int H, int CPL>
+constexpr WinKernel win64_pick() {
+    if constexpr (CPL == 1 && H >= 7) return &getrf_win2_kernel<H, win_pf(H)>;
+    else return &getrf_win64_kernel<H, CPL, win_pf(H)>;
+}
+
 template <int CPL, int LO, int HI>
 struct Win64Range {
     template <int... Is>
     static constexpr auto make(std::integer_sequence<int, Is...>) {
-        return std::array<WinKernel, HI - LO + 1>{
-            {&getrf_win64_kernel<LO + Is, CPL, win_pf(LO + Is)>...}};
+        return std::array<WinKernel, HI - LO + 1>{{win64_pick<LO + Is, CPL>()...}};
     }
 };
 

@@ -126,21 +126,50 @@ __global__ __launch_bounds__(64) void getrs_kernel(RsParams P) {
     }
 }
 
-// Register-window solve for narrow bands (kl <= 63, kl + ku < 64 * CPL).
-// Forward: row r of the right-hand side lives in lane r mod 64; at step j lane
-// j mod 64 holds b[j], the swap with row ipiv[j]-1 is an exchange between two
-// lanes, and lanes holding rows j+1..j+kl apply one fma each.  Backward: row r
-// lives in lane r mod 64, register sub-slot (r / 64) mod CPL; at step j the
-// lane holding b[j] divides by U(j,j) and lanes holding rows j-kl-ku..j-1 apply
-// one fma each.  Multipliers, U entries, pivot indices and rows entering the
-// window are loaded D steps ahead into register rings whose index is a
-// compile-time constant (the step loop is unrolled by 64 * CPL).  Every step is
-// straight-line code: memory goes through range-checked buffer operations and
-// lane predicates are selects, so the prefetch ring stays in flight.
+// Register-window solve for narrow bands (kl <= 63, kl + ku < 64 * CPL), one
+// wavefront per right-hand side.  Each step costs a few instructions: the
+// right-hand side row the step finishes is read from its lane, and the rows
+// it updates apply one fused multiply-add under a lane mask that the scalar
+// unit rotates by one lane per step.
+//
+// Forward: row r lives in lane r mod 64.  Step j reads b[j] from lane j mod 64
+// (after the interchange with row ipiv[j]-1, an exchange between two lanes),
+// lanes j+1..j+kl (mod 64) apply the multipliers of column j, lane j mod 64
+// stores the finished row and takes row j+64.  Backward: row r lives in lane
+// (n-1-r) mod 64, register slot ((n-1-r) / 64) mod CPL.  Step j divides the
+// row by U(j,j), the rows j-kl-ku..j-1 apply the column of U, and the slot
+// stores row j and takes row j - 64*CPL.  Columns of L and U are loaded 64
+// steps ahead into a register ring, the rows that enter in one block of
+// steps with one load; the step loop is unrolled by 64 * CPL so that every
+// register index is a compile-time constant.
+
+template <int START>
+__device__ __forceinline__ unsigned long long rotl64(unsigned long long w) {
+    constexpr int s = START & 63;
+    if constexpr (s == 0) return w;
+    else return (w << s) | (w >> (64 - s));
+}
+
+// lanes (START .. START+len-1) mod (64 * CPL) as CPL 64-bit words (len < 64 * CPL)
+template <int CPL, int START>
+__device__ __forceinline__ unsigned long long window_word(int len, int word) {
+    if constexpr (CPL == 1) {
+        const unsigned long long ones = len >= 64 ? ~0ull : ((1ull << len) - 1);
+        return rotl64<START>(ones);
+    } else {
+        typedef unsigned __int128 u128;
+        constexpr int s = START & 127;
+        const u128 ones = (u128(1) << len) - 1;
+        u128 w = ones;
+        if constexpr (s != 0) w = (ones << s) | (ones >> (128 - s));
+        return (unsigned long long)(word == 0 ? w : (w >> 64));
+    }
+}
+
 template <int CPL>
 __global__ __launch_bounds__(64) void getrs_win_kernel(RsParams P) {
-    constexpr int D = 16;
     constexpr int M = 64 * CPL;
+    constexpr int DB = 64 / CPL;  // backward ring depth per slot
     const int L = threadIdx.x;
     const int64_t sys = blockIdx.x;
     const int64_t bidx = sys / P.nrhs, k = sys - bidx * P.nrhs;
@@ -152,114 +181,109 @@ __global__ __launch_bounds__(64) void getrs_win_kernel(RsParams P) {
 
     // ------------------------------------------------------------ forward --
     if (kl > 0 && n > 1) {
-        double bv = buf_ld(xb, L <= kl ? rowoff(L) : kOutside);
-        auto loff = [&](int j) -> uint32_t {  // multiplier for this lane's row at step j
-            const int t = (L - j) & 63;
-            const bool ok = j < n - 1 && t >= 1 && t <= min(kl, n - 1 - j);
-            return ok ? uint32_t(j * ldab + kv + t) * 8u : kOutside;
-        };
-        double lr[D], rr[D];
-#pragma unroll
-        for (int d = 0; d < D; ++d) {
-            lr[d] = buf_ld(ab, loff(d));
-            rr[d] = buf_ld(xb, rowoff(kl + 1 + d));
-        }
+        double bv = buf_ld(xb, rowoff(L));
+        double nxt = buf_ld(xb, rowoff(64 + L));
         int ipv = buf_ld_i32(pb, uint32_t(L) * 4u);
-        int ipv_next = buf_ld_i32(pb, uint32_t(L + 64) * 4u);
+        double lr[64];
+        // the multiplier of column j for the row in lane L sits kv + ((L - j) mod 64)
+        // entries into column j (the lanes outside the window read values they ignore)
+        // (the column base, or an offset past every buffer, is chosen on the scalar
+        // unit and added to the lane's part: the whole offset is range-checked)
+        auto loff = [&](int u, int j) -> uint32_t {
+            return uint32_t(kv + ((L - u) & 63)) * 8u + (j < n ? uint32_t(j * ldab) * 8u : kOutside);
+        };
+#pragma unroll
+        for (int u = 0; u < 64; ++u) lr[u] = buf_ld(ab, loff(u, u));
         for (int j0 = 0; j0 < n - 1; j0 += 64) {
+            const int ipv_next = buf_ld_i32(pb, uint32_t(j0 + 64 + L) * 4u);
+            const double nxt_next = buf_ld(xb, rowoff(j0 + 128 + L));
+            double done = 0.0;  // lane u: row j0 + u once step j0 + u has made it final
             [&]<int... Us>(std::integer_sequence<int, Us...>) {
                 (
                     [&] {
                         constexpr int u = Us;
                         const int j = j0 + u;
-                        const bool live = j < n - 1;
-                        int l = __builtin_amdgcn_readlane(ipv, u) - 1;
-                        l = (live && l > j && l <= j + kl && l < n) ? l : j;
-                        if (l != j) {
-                            const int ls = l & 63;
+                        if (j >= n - 1) return;
+                        const int p = __builtin_amdgcn_readlane(ipv, u) - 1;
+                        if (unsigned(p - j - 1) < unsigned(min(kl, n - 1 - j))) {
+                            const int ls = p & 63;
                             const double vj = readlane_d(bv, u);
-                            const double vl = readlane_d(bv, ls);
-                            bv = L == u ? vl : (L == ls ? vj : bv);
+                            const double vp = readlane_d(bv, ls);
+                            bv = L == u ? vp : (L == ls ? vj : bv);
                         }
                         const double bj = readlane_d(bv, u);
-                        const int t = (L - u) & 63;
-                        const bool m = t >= 1 && t <= min(kl, n - 1 - j);
-                        const double nb = __builtin_fma(-lr[u % D], bj, bv);
-                        bv = m ? nb : bv;
-                        buf_st(xb, (L == u && live) ? rowoff(j) : kOutside, bv);  // row j is final
-                        const int renter = j + kl + 1;
-                        bv = (live && L == (renter & 63) && renter < n) ? rr[u % D] : bv;
-                        lr[u % D] = buf_ld(ab, loff(j + D));
-                        rr[u % D] = buf_ld(xb, rowoff(renter + D));
-                        if constexpr (u == 63) {
-                            ipv = ipv_next;
-                            ipv_next = buf_ld_i32(pb, uint32_t(j0 + 128 + L) * 4u);
+                        const int km = min(kl, n - 1 - j);
+                        if (__builtin_amdgcn_inverse_ballot_w64(window_word<1, u + 1>(km, 0)))
+                            bv = __builtin_fma(-lr[u], bj, bv);
+                        if (__builtin_amdgcn_inverse_ballot_w64(1ull << u)) {
+                            done = bv;  // row j is final
+                            bv = nxt;   // row j + 64 enters
                         }
+                        lr[u] = buf_ld(ab, loff(u, j + 64));
                     }(),
                     ...);
             }(std::make_integer_sequence<int, 64>{});
+            // rows j0 .. j0+63 that are final (row n-1 is stored after the loop)
+            buf_st(xb, j0 + L < n - 1 ? rowoff(j0 + L) : kOutside, done);
+            ipv = ipv_next;
+            nxt = nxt_next;
         }
         buf_st(xb, L == ((n - 1) & 63) ? rowoff(n - 1) : kOutside, bv);
         __threadfence();
     }
     // ----------------------------------------------------------- backward --
     {
-        auto rowof = [&](int s, int j) -> int { return j - ((j - (L + 64 * s)) & (M - 1)); };
-        double bv[CPL];
+        // slot s of lane L holds row n-1 - (L + 64 s) - M*q for block q
+        double bv[CPL], nxt[CPL];
 #pragma unroll
-        for (int s = 0; s < CPL; ++s) {
-            const int r = rowof(s, n - 1);
-            bv[s] = buf_ld(xb, r >= n - 1 - kv ? rowoff(r) : kOutside);
-        }
-        auto uoff = [&](int s, int j) -> uint32_t {  // U(row, j) for this lane's row at step j
-            const int t = j - rowof(s, j);
-            const bool ok = j >= 0 && t >= 1 && t <= min(kv, j);
-            return ok ? uint32_t(j * ldab + kv - t) * 8u : kOutside;
+        for (int s = 0; s < CPL; ++s) bv[s] = buf_ld(xb, rowoff(n - 1 - (L + 64 * s)));
+        double ur[CPL][DB];
+        // entry (j - t, j) of U, t = ((L + 64 s - m) mod M), sits kv - t entries into column j
+        // (for lanes beyond the band kv - t is negative and the offset wraps to
+        // some other entry of the range-checked buffer; those lanes are never used)
+        auto uoff = [&](int s, int u, int j) -> uint32_t {
+            return uint32_t(kv - ((L + 64 * s - u) & (M - 1))) * 8u +
+                   (j >= 0 ? uint32_t(j * ldab) * 8u : kOutside);
         };
-        auto doff = [&](int j) -> uint32_t { return j >= 0 ? uint32_t(j * ldab + kv) * 8u : kOutside; };
-        double ur[CPL][D], dr[D], rr[D];
 #pragma unroll
-        for (int d = 0; d < D; ++d) {
+        for (int d = 0; d < DB; ++d)
 #pragma unroll
-            for (int s = 0; s < CPL; ++s) ur[s][d] = buf_ld(ab, uoff(s, n - 1 - d));
-            dr[d] = buf_ld(ab, doff(n - 1 - d));
-            rr[d] = buf_ld(xb, rowoff(n - 2 - kv - d));
-        }
-        // steps are counted from the end so that register indices are constants
+            for (int s = 0; s < CPL; ++s) ur[s][d] = buf_ld(ab, uoff(s, d, n - 1 - d));
         for (int m0 = 0; m0 < n; m0 += M) {
+            double done[CPL];
+#pragma unroll
+            for (int s = 0; s < CPL; ++s) {
+                nxt[s] = buf_ld(xb, rowoff(n - 1 - (m0 + M + L + 64 * s)));
+                done[s] = 0.0;
+            }
             [&]<int... Us>(std::integer_sequence<int, Us...>) {
                 (
                     [&] {
                         constexpr int u = Us;
+                        constexpr int lj = u & 63, sj = u >> 6;
                         const int j = n - 1 - (m0 + u);
-                        const bool live = j >= 0;
-                        const int lj = j & 63;
-                        const int sj = (j >> 6) & (CPL - 1);
-                        double zs = bv[0];
-#pragma unroll
-                        for (int s = 1; s < CPL; ++s) zs = sj == s ? bv[s] : zs;
-                        const double z = zs / dr[u % D];
+                        if (j < 0) return;
+                        const double z = bv[sj] / ur[sj][u % DB];
                         const double xj = readlane_d(z, lj);
-                        buf_st(xb, (live && L == lj) ? rowoff(j) : kOutside, xj);
+                        const int tm = min(kv, j);
 #pragma unroll
                         for (int s = 0; s < CPL; ++s) {
-                            const int t = j - rowof(s, j);
-                            const bool m = t >= 1 && t <= min(kv, j);
-                            const double nb = __builtin_fma(-ur[s][u % D], xj, bv[s]);
-                            bv[s] = m ? nb : bv[s];
+                            if (__builtin_amdgcn_inverse_ballot_w64(window_word<CPL, u + 1>(tm, s)))
+                                bv[s] = __builtin_fma(-ur[s][u % DB], xj, bv[s]);
                         }
-                        const int renter = j - 1 - kv;
-                        const bool ent = live && renter >= 0 && L == (renter & 63);
-                        const int se = (renter >> 6) & (CPL - 1);
+                        if (__builtin_amdgcn_inverse_ballot_w64(1ull << lj)) {
+                            done[sj] = xj;       // row j is final
+                            bv[sj] = nxt[sj];    // row j - M enters
+                        }
 #pragma unroll
-                        for (int s = 0; s < CPL; ++s) bv[s] = (ent && se == s) ? rr[u % D] : bv[s];
-#pragma unroll
-                        for (int s = 0; s < CPL; ++s) ur[s][u % D] = buf_ld(ab, uoff(s, j - D));
-                        dr[u % D] = buf_ld(ab, doff(j - D));
-                        rr[u % D] = buf_ld(xb, rowoff(renter - D));
+                        for (int s = 0; s < CPL; ++s)
+                            ur[s][u % DB] = buf_ld(ab, uoff(s, u + DB, j - DB));
                     }(),
                     ...);
             }(std::make_integer_sequence<int, M>{});
+            // rows n-1-m0 .. n-M-m0 are final
+#pragma unroll
+            for (int s = 0; s < CPL; ++s) buf_st(xb, rowoff(n - 1 - (m0 + L + 64 * s)), done[s]);
         }
     }
 }
