@@ -237,7 +237,11 @@ int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
         WinKernel k;
         int per_wave;
         if (v == BANDLU_GETRF_WINDOW_G16) {
-            k = win_kernel(16, need <= 16 ? 1 : 2, H);
+            // one column per lane addresses the whole batch through one
+            // range-checked buffer: it must stay below 2 GiB
+            const bool one = need <= 16 && batch * strideAB * 8 <= kMaxBufferBytes &&
+                             batch * strideP * 4 <= kMaxBufferBytes;
+            k = win_kernel(16, one ? 1 : 2, H);
             per_wave = 4;
         } else {
             k = win_kernel(64, need <= 64 ? 1 : 2, H);

@@ -1,0 +1,153 @@
+// Batched banded LU with partial pivoting (xGBTRF semantics) for small
+// bands: sixteen lanes per matrix, four matrices per wavefront, all four at
+// the same column step (Sec. III-A's specialised algorithm f(N), the batched
+// form).  kl <= 7 and 2kl+ku+1 <= 16.
+//
+// Lane i of a group holds column c == i (mod 16) of its matrix's band window;
+// the window rows of that column live in sixteen register slots (row mod 16),
+// of which kl+1 are active.  With the step loop unrolled by 16, the lane that
+// holds column j and the slot of row j are compile-time constants, so the
+// pivot, the pivot offset and the multipliers reach the other lanes of a
+// group by one DPP row broadcast each (row_newbcast), with no LDS traffic.
+// The four matrices pivot independently: the row interchange is a chain of
+// selects on the group's pivot offset, and the update runs under a per-lane
+// exec mask.  All loads and stores go through one range-checked buffer over
+// the whole batch, so each step is branch-free and a 16-step prefetch ring
+// stays in flight.  Every entry sees the same fused multiply-adds, in the same
+// order, as in the unblocked algorithm.
+#pragma once
+
+#include <cfloat>
+#include <utility>
+
+#include "bufio.hpp"
+#include "common.hpp"
+#include "getrf_window.hpp"
+
+namespace bandlu {
+
+// value of lane K of this lane's row of 16
+template <int K>
+__device__ __forceinline__ int row_bcast_i(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, 0x150 + K, 0xf, 0xf, false);
+}
+
+template <int K>
+__device__ __forceinline__ double row_bcast_d(double v) {
+    const long long x = __double_as_longlong(v);
+    const int lo = row_bcast_i<K>((int)(x & 0xffffffffll));
+    const int hi = row_bcast_i<K>((int)(x >> 32));
+    return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+}
+
+template <int H>
+__global__ __launch_bounds__(64) void getrf_g16_kernel(WinParams P) {
+    static_assert(H >= 1 && H <= 8, "kl <= 7");
+    constexpr int kl = H - 1;
+    constexpr int PF = 16;
+    const int lane = threadIdx.x;
+    const int gl = lane & 15;
+    const int b = blockIdx.x * 4 + (lane >> 4);
+    const bool live = b < P.batch;
+    const int n = P.n, ku = P.ku, kv = kl + P.ku, ldab = int(P.ldab);
+    // one buffer over the whole batch (the host checks that it is < 2 GiB)
+    const Buf ab = make_buf(P.AB, uint32_t(int64_t(P.batch) * P.strideAB * 8));
+    const Buf pb = make_buf(P.ipiv, uint32_t(int64_t(P.batch) * P.strideP * 4));
+    const uint32_t mbase = live ? uint32_t(int64_t(b) * P.strideAB * 8) : kOutside;
+    const uint32_t pbase = live ? uint32_t(int64_t(b) * P.strideP * 4) : kOutside;
+
+    // the column in [x, x+16) this lane holds
+    auto colof = [&](int x) -> int { return x + ((gl - x) & 15); };
+    // original band entry (r, c) of this lane's matrix, else outside
+    auto foff = [&](int r, int c) -> uint32_t {
+        const bool ok = c >= 0 && c < n && r >= 0 && r < n && unsigned(r - c + ku) <= unsigned(kv);
+        return ok ? mbase + uint32_t(c * ldab + kv + r - c) * 8u : kOutside;
+    };
+
+    double a[16];
+    double pf[PF];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) a[r] = r < H ? buf_ld(ab, foff(r, colof(r - H + 1))) : 0.0;
+#pragma unroll
+    for (int k = 0; k < PF; ++k) pf[k] = buf_ld(ab, foff(k + H, colof(k + 1)));
+    int ju = 0, info = 0;
+
+    auto step = [&]<int U>(int j) __attribute__((always_inline)) {
+        constexpr int S0 = U;  // slot of row j; lane U of each group holds column j
+        const int km = min(kl, n - 1 - j);
+        const int c = colof(j);
+        // ---- 1. pivot: the lane of column j scans its kl+1 rows (first
+        // largest |a|; a NaN counts only in first position), then its
+        // group takes the offset and the value from it
+        double best = a[S0], bk = __builtin_isnan(best) ? __builtin_inf() : fabs(best);
+        int pl = 0;
+#pragma unroll
+        for (int t = 1; t < H; ++t) {
+            const double v = a[(S0 + t) & 15];
+            const bool gt = t <= km && fabs(v) > bk;  // false for a NaN
+            bk = gt ? fabs(v) : bk;
+            best = gt ? v : best;
+            pl = gt ? t : pl;
+        }
+        const int p = row_bcast_i<U>(pl);
+        const double piv = row_bcast_d<U>(best);
+        buf_st_i32(pb, gl == U ? pbase + uint32_t(j) * 4u : kOutside, j + p + 1);
+        const bool elim = piv != 0.0;
+        info = (!elim && info == 0) ? j + 1 : info;
+        if (elim) {
+            ju = max(ju, min(j + ku + p, n - 1));
+            // ---- 2. interchange rows j and j+p in columns j..ju
+            if constexpr (H > 1) {
+                if (c <= ju) {
+                    double a0 = a[S0];
+#pragma unroll
+                    for (int k = 1; k < H; ++k) {
+                        const bool hit = p == k;
+                        const double ak = a[(S0 + k) & 15];
+                        a0 = hit ? ak : a0;
+                        a[(S0 + k) & 15] = hit ? a[S0] : ak;
+                    }
+                    a[S0] = a0;
+                }
+                // ---- 3. multipliers, formed in the lane of column j
+                if (gl == U) {
+                    if (fabs(piv) >= DBL_MIN) {
+                        const double rcp = 1.0 / piv;
+#pragma unroll
+                        for (int t = 1; t < H; ++t) a[(S0 + t) & 15] = a[(S0 + t) & 15] * rcp;
+                    } else {
+#pragma unroll
+                        for (int t = 1; t < H; ++t) a[(S0 + t) & 15] = a[(S0 + t) & 15] / piv;
+                    }
+                }
+                // ---- 4. rank-1 update of columns j+1..ju
+                double lm[H];
+#pragma unroll
+                for (int t = 1; t < H; ++t) lm[t] = row_bcast_d<U>(a[(S0 + t) & 15]);
+                if (c > j && c <= ju) {
+                    const double uu = a[S0];
+#pragma unroll
+                    for (int t = 1; t < H; ++t) a[(S0 + t) & 15] = __builtin_fma(-lm[t], uu, a[(S0 + t) & 15]);
+                }
+            }
+        }
+        // ---- 5. row j leaves (U row j for active columns, a multiplier for
+        // retired ones); row j+H enters its slot from the prefetch ring
+        {
+            const int co = colof(j - H + 1);
+            const bool ok = co < n && j >= co - kv;
+            buf_st(ab, ok ? mbase + uint32_t(co * ldab + kv + j - co) * 8u : kOutside, a[S0]);
+            a[(S0 + H) & 15] = pf[U];
+            pf[U] = buf_ld(ab, foff(j + PF + H, colof(j + PF + 1)));
+        }
+    };
+
+    for (int j0 = 0; j0 < n; j0 += PF) {
+        [&]<int... Us>(std::integer_sequence<int, Us...>) {
+            ((j0 + Us < n ? step.template operator()<Us>(j0 + Us) : (void)0), ...);
+        }(std::make_integer_sequence<int, PF>{});
+    }
+    if (live && gl == 0) P.info[b] = info;
+}
+
+}  // namespace bandlu

@@ -288,6 +288,148 @@ __global__ __launch_bounds__(64) void getrs_win_kernel(RsParams P) {
     }
 }
 
+// Batched solve for small bands (kl + ku <= 15): sixteen lanes per system,
+// four systems per wavefront, all at the same step.  Row r of a right-hand
+// side lives in lane r mod 16 of its group (forward) or lane (n-1-r) mod 16
+// (backward); with the step loop unrolled by 16 the lane of the row a step
+// finishes is a compile-time constant, so its value reaches the rest of the
+// group by one DPP row broadcast.  The row interchange of the forward pass is
+// a chain of selects over the group's pivot offset (skipped when no system
+// of the wavefront pivots at that step).  One range-checked buffer per array
+// spans the whole batch (the host checks that each is < 2 GiB).
+template <int K>
+__device__ __forceinline__ double rs_bcast(double v) {
+    const long long x = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(x & 0xffffffffll), 0x150 + K, 0xf, 0xf, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(x >> 32), 0x150 + K, 0xf, 0xf, false);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+}
+
+template <int K>
+__device__ __forceinline__ int rs_bcast_i(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, 0x150 + K, 0xf, 0xf, false);
+}
+
+// the 16-bit lane pattern `bits` (bit i = lane i of a group) in every group
+__device__ __forceinline__ unsigned long long rs_groups(unsigned bits) {
+    return 0x0001000100010001ull * (bits & 0xffffu);
+}
+
+__global__ __launch_bounds__(64) void getrs_g16_kernel(RsParams P, int64_t systems) {
+    const int lane = threadIdx.x, gl = lane & 15;
+    const int64_t sys = int64_t(blockIdx.x) * 4 + (lane >> 4);
+    const bool live = sys < systems;
+    const int64_t bidx = live ? sys / P.nrhs : 0, k = live ? sys - bidx * P.nrhs : 0;
+    const int n = int(P.n), kl = int(P.kl), kv = int(P.kl + P.ku), ldab = int(P.ldab);
+    const int64_t batch = (systems + P.nrhs - 1) / P.nrhs;
+    const Buf ab = make_buf(P.AB, uint32_t(batch * P.strideAB * 8));
+    const Buf pb = make_buf(P.ipiv, uint32_t(batch * P.strideP * 4));
+    const Buf xb = make_buf(P.B, uint32_t(batch * P.strideB * 8));
+    const uint32_t abase = live ? uint32_t(bidx * P.strideAB * 8) : kOutside;
+    const uint32_t pbase = live ? uint32_t(bidx * P.strideP * 4) : kOutside;
+    const uint32_t xbase = live ? uint32_t((bidx * P.strideB + k * P.ldb) * 8) : kOutside;
+    auto rowoff = [&](int r) -> uint32_t { return r >= 0 && r < n ? xbase + uint32_t(r) * 8u : kOutside; };
+
+    // ------------------------------------------------------------ forward --
+    if (kl > 0 && n > 1) {
+        double bv = buf_ld(xb, rowoff(gl));
+        double nxt = buf_ld(xb, rowoff(16 + gl));
+        int ipv = buf_ld_i32(pb, gl < n ? pbase + uint32_t(gl) * 4u : kOutside);
+        double lr[16];
+        // multiplier of column j for the row in lane gl: kv + ((gl - j) mod 16) into column j
+        auto loff = [&](int u, int j) -> uint32_t {
+            return j < n ? abase + uint32_t(j * ldab + kv + ((gl - u) & 15)) * 8u : kOutside;
+        };
+#pragma unroll
+        for (int u = 0; u < 16; ++u) lr[u] = buf_ld(ab, loff(u, u));
+        for (int j0 = 0; j0 < n - 1; j0 += 16) {
+            const int ipv_next =
+                buf_ld_i32(pb, j0 + 16 + gl < n ? pbase + uint32_t(j0 + 16 + gl) * 4u : kOutside);
+            const double nxt_next = buf_ld(xb, rowoff(j0 + 32 + gl));
+            double done = 0.0;
+            [&]<int... Us>(std::integer_sequence<int, Us...>) {
+                (
+                    [&] {
+                        constexpr int u = Us;
+                        const int j = j0 + u;
+                        if (j >= n - 1) return;
+                        const int km = min(kl, n - 1 - j);
+                        const int toff = (gl - u) & 15;
+                        const int d = rs_bcast_i<u>(ipv) - 1 - j;  // pivot offset of this group
+                        if (__ballot(d != 0)) {
+                            // exchange rows j and j+d (0 < d <= km) inside each group
+                            const double bj0 = rs_bcast<u>(bv);
+                            double bjn = bj0;
+                            [&]<int... Ts>(std::integer_sequence<int, Ts...>) {
+                                (
+                                    [&] {
+                                        constexpr int t = Ts + 1;
+                                        if (t <= kl) {
+                                            const double vt = rs_bcast<(u + t) & 15>(bv);
+                                            bjn = d == t ? vt : bjn;
+                                        }
+                                    }(),
+                                    ...);
+                            }(std::make_integer_sequence<int, 15>{});
+                            const bool ok = d > 0 && d <= km;
+                            bv = (ok && toff == 0) ? bjn : ((ok && toff == d) ? bj0 : bv);
+                        }
+                        const double bj = rs_bcast<u>(bv);
+                        if (__builtin_amdgcn_inverse_ballot_w64(rs_groups(((1u << km) - 1) << (u + 1) |
+                                                                          ((1u << km) - 1) >> (15 - u))))
+                            bv = __builtin_fma(-lr[u], bj, bv);
+                        if (__builtin_amdgcn_inverse_ballot_w64(rs_groups(1u << u))) {
+                            done = bv;  // row j is final
+                            bv = nxt;   // row j + 16 enters
+                        }
+                        lr[u] = buf_ld(ab, loff(u, j + 16));
+                    }(),
+                    ...);
+            }(std::make_integer_sequence<int, 16>{});
+            buf_st(xb, j0 + gl < n - 1 ? rowoff(j0 + gl) : kOutside, done);
+            ipv = ipv_next;
+            nxt = nxt_next;
+        }
+        buf_st(xb, gl == ((n - 1) & 15) ? rowoff(n - 1) : kOutside, bv);
+        __threadfence();
+    }
+    // ----------------------------------------------------------- backward --
+    {
+        double bv = buf_ld(xb, rowoff(n - 1 - gl));
+        double ur[16];
+        // entry (j - t, j) of U, t = (gl - m) mod 16, sits kv - t entries into column j
+        auto uoff = [&](int u, int j) -> uint32_t {
+            return j >= 0 ? abase + uint32_t(j * ldab + kv - ((gl - u) & 15)) * 8u : kOutside;
+        };
+#pragma unroll
+        for (int u = 0; u < 16; ++u) ur[u] = buf_ld(ab, uoff(u, n - 1 - u));
+        for (int m0 = 0; m0 < n; m0 += 16) {
+            const double nxt = buf_ld(xb, rowoff(n - 1 - (m0 + 16 + gl)));
+            double done = 0.0;
+            [&]<int... Us>(std::integer_sequence<int, Us...>) {
+                (
+                    [&] {
+                        constexpr int u = Us;
+                        const int j = n - 1 - (m0 + u);
+                        if (j < 0) return;
+                        const double xj = rs_bcast<u>(bv / ur[u]);
+                        const int tm = min(kv, j);
+                        if (__builtin_amdgcn_inverse_ballot_w64(rs_groups(((1u << tm) - 1) << (u + 1) |
+                                                                          ((1u << tm) - 1) >> (15 - u))))
+                            bv = __builtin_fma(-ur[u], xj, bv);
+                        if (__builtin_amdgcn_inverse_ballot_w64(rs_groups(1u << u))) {
+                            done = xj;  // row j is final
+                            bv = nxt;   // row j - 16 enters
+                        }
+                        ur[u] = buf_ld(ab, uoff(u, j - 16));
+                    }(),
+                    ...);
+            }(std::make_integer_sequence<int, 16>{});
+            buf_st(xb, rowoff(n - 1 - (m0 + gl)), done);
+        }
+    }
+}
+
 template <int W>
 constexpr int rs_depth() { return W >= 16 ? 2 : 32 / W; }
 
@@ -328,6 +470,15 @@ int launch_getrs(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *
         return BANDLU_ERR_UNSUPPORTED;
     }
     const bool buf_ok = ldab * n * 8 <= kMaxBufferBytes && n * 8 <= kMaxBufferBytes;
+    // many systems with a small band: sixteen lanes per system
+    if (systems >= 64 && kl + ku <= 15 && batch * strideAB * 8 <= kMaxBufferBytes &&
+        batch * strideP * 4 <= kMaxBufferBytes && batch * strideB * 8 <= kMaxBufferBytes &&
+        ldb * nrhs <= strideB) {
+        hipLaunchKernelGGL(getrs_g16_kernel, dim3((unsigned)((systems + 3) / 4)), dim3(64), 0, s, P,
+                           systems);
+        BANDLU_CHECK_LAUNCH("band_getrs (16 lanes per system)");
+        return BANDLU_OK;
+    }
     if (buf_ok && kl <= 63 && kl + ku < 64) {
         hipLaunchKernelGGL(getrs_win_kernel<1>, dim3((unsigned)systems), dim3(64), 0, s, P);
         BANDLU_CHECK_LAUNCH("band_getrs (window)");
