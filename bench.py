@@ -49,8 +49,8 @@ def kernel_costs(n, kl, ku, batch):
 STEP_SOURCES = {
     "detect": ["detect.hip", "common.hpp"],
     "convert": ["convert.hip", "common.hpp"],
-    "getrf": ["getrf.hip", "getrf_win64.hpp", "getrf_window.hpp", "getrf_blocked.hip", "bufio.hpp",
-              "common.hpp"],
+    "getrf": ["getrf.hip", "getrf_win64.hpp", "getrf_win2.hpp", "getrf_window.hpp", "getrf_g16.hpp",
+              "getrf_blocked.hip", "getrf_mfma.hip", "wave.hpp", "bufio.hpp", "common.hpp"],
     "getrs": ["getrs.hip", "bufio.hpp", "common.hpp"],
 }
 
