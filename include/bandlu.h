@@ -192,6 +192,34 @@ int band_getrf_ex(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab, 
                   int32_t *d_ipiv, int64_t strideP, int32_t *d_info, int64_t batch, int variant,
                   void *stream);
 
+/*
+ * band_getrs_variant -- which solve kernel band_getrs(_batched) runs for these
+ * sizes, with contiguous arguments (ldab = 2kl+ku+1, ldb = n; host-only,
+ * enqueues nothing).  Returns one of the BANDLU_GETRS_* codes below, or a
+ * negative status for invalid sizes.
+ */
+#define BANDLU_GETRS_WINDOW 1  /* register window, one wavefront per right-hand side   */
+#define BANDLU_GETRS_G16 2     /* register window, 16 lanes per system, many systems    */
+#define BANDLU_GETRS_RING 3    /* register ring plus factor columns staged in LDS       */
+#define BANDLU_GETRS_GENERIC 4 /* right-hand side in LDS or global memory, any band     */
+int band_getrs_variant(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, int64_t batch);
+
+/*
+ * band_getrs_ex -- band_getrs_batched with the kernel chosen by the caller:
+ * variant 0 picks it as band_getrs_batched does, 1..4 forces that
+ * BANDLU_GETRS_* kernel.  Arguments 1-13 as in band_getrs_batched (argument
+ * 14 is the variant).  Every variant computes the same sequence of
+ * operations, so the results are bitwise equal.  A variant that cannot handle
+ * the sizes (a window for kl > 63 or kl+ku >= 128, sixteen lanes for
+ * kl+ku > 15, the ring for kl+ku > 1023 or a band of 2 GiB or more) returns
+ * BANDLU_ERR_UNSUPPORTED and enqueues nothing.  For tests and measurements
+ * that compare the kernels on one input.
+ */
+int band_getrs_ex(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *dAB,
+                  int64_t ldab, int64_t strideAB, const int32_t *d_ipiv, int64_t strideP,
+                  double *dB, int64_t ldb, int64_t strideB, int64_t batch, int variant,
+                  void *stream);
+
 /* Text for a status code (static storage). */
 const char *band_status_string(int status);
 

@@ -48,6 +48,9 @@ EXPORTS = {
                            _i64, _vp],
     "band_getrf_variant": [_i64, _i64, _i64, _i64],
     "band_getrf_ex": [_i64, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _vp, _i64, ctypes.c_int, _vp],
+    "band_getrs_variant": [_i64, _i64, _i64, _i64, _i64],
+    "band_getrs_ex": [_i64, _i64, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _vp, _i64, _i64, _i64,
+                      ctypes.c_int, _vp],
     "band_status_string": [ctypes.c_int],
     "band_last_error": [],
 }
@@ -59,6 +62,8 @@ for _name, _args in EXPORTS.items():
 
 VARIANTS = {1: "window", 2: "window_g16", 3: "generic", 4: "blocked", 5: "blocked_mfma"}
 _VARIANT_CODES = {name: code for code, name in VARIANTS.items()}
+GETRS_VARIANTS = {1: "window", 2: "g16", 3: "ring", 4: "generic"}
+_GETRS_CODES = {name: code for code, name in GETRS_VARIANTS.items()}
 
 
 class BandLUError(RuntimeError):
@@ -210,20 +215,38 @@ def band_getrf_variant(n, kl, ku, batch=1):
 
 
 # ------------------------------------------------------------------- getrs --
-def band_getrs(AB, kl, ku, ipiv, B):
-    """Solve in place; B has shape (nrhs, ldb) with B[k, i] = row i of rhs k."""
+def _getrs_code(variant):
+    if variant not in _GETRS_CODES:
+        raise ValueError(f"unknown solve variant {variant!r}; one of {sorted(_GETRS_CODES)}")
+    return _GETRS_CODES[variant]
+
+
+def band_getrs(AB, kl, ku, ipiv, B, variant=None):
+    """Solve in place; B has shape (nrhs, ldb) with B[k, i] = row i of rhs k.
+    ``variant`` (a name from GETRS_VARIANTS) forces a kernel through band_getrs_ex."""
     _check(AB, torch.float64, "AB", 2)
     _check(ipiv, torch.int32, "ipiv", 1)
     _check(B, torch.float64, "B", 2)
     n = AB.shape[0]
     nrhs = B.shape[0]
     ldb = max(_ld(B), n, 1)
-    _call("band_getrs", n, kl, ku, nrhs, _ptr(AB), max(_ld(AB), 1), _ptr(ipiv), _ptr(B), ldb,
-          _stream())
+    ldab = max(_ld(AB), 1)
+    if variant is None:
+        _call("band_getrs", n, kl, ku, nrhs, _ptr(AB), ldab, _ptr(ipiv), _ptr(B), ldb, _stream())
+    else:
+        _call("band_getrs_ex", n, kl, ku, nrhs, _ptr(AB), ldab, ldab * n, _ptr(ipiv), n, _ptr(B),
+              ldb, ldb * nrhs, 1, _getrs_code(variant), _stream())
     return B
 
 
-def band_getrs_batched(AB, kl, ku, ipiv, B):
+def band_getrs_variant(n, kl, ku, nrhs=1, batch=1):
+    v = _lib.band_getrs_variant(n, kl, ku, nrhs, batch)
+    if v < 0:
+        raise BandLUError("band_getrs_variant", v)
+    return GETRS_VARIANTS[v]
+
+
+def band_getrs_batched(AB, kl, ku, ipiv, B, variant=None):
     """Batched solve in place; B has shape (batch, nrhs, ldb)."""
     _check(AB, torch.float64, "AB", 3)
     _check(ipiv, torch.int32, "ipiv", 2)
@@ -235,8 +258,12 @@ def band_getrs_batched(AB, kl, ku, ipiv, B):
     sAB = AB.stride(0) if batch > 1 else ldab * n
     sP = ipiv.stride(0) if batch > 1 else n
     sB = B.stride(0) if batch > 1 else ldb * nrhs
-    _call("band_getrs_batched", n, kl, ku, nrhs, _ptr(AB), ldab, sAB, _ptr(ipiv), sP, _ptr(B),
-          ldb, sB, batch, _stream())
+    if variant is None:
+        _call("band_getrs_batched", n, kl, ku, nrhs, _ptr(AB), ldab, sAB, _ptr(ipiv), sP, _ptr(B),
+              ldb, sB, batch, _stream())
+    else:
+        _call("band_getrs_ex", n, kl, ku, nrhs, _ptr(AB), ldab, sAB, _ptr(ipiv), sP, _ptr(B), ldb,
+              sB, batch, _getrs_code(variant), _stream())
     return B
 
 

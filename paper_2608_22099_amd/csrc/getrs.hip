@@ -14,6 +14,12 @@
 #include <utility>
 
 namespace bandlu {
+
+int launch_getrs_ring(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *dAB,
+                      int64_t ldab, int64_t strideAB, const int32_t *d_ipiv, int64_t strideP,
+                      double *dB, int64_t ldb, int64_t strideB, int64_t batch, hipStream_t s);
+bool getrs_ring_fits(int64_t n, int64_t kl, int64_t ku, int64_t ldab);
+
 namespace {
 
 struct RsParams {
@@ -447,9 +453,31 @@ int launch_w(bool lds, const RsParams &P, int64_t systems, hipStream_t s) {
     return BANDLU_OK;
 }
 
+bool g16_fits(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, int64_t strideAB, int64_t strideP,
+              int64_t ldb, int64_t strideB, int64_t batch) {
+    return kl + ku <= 15 && batch * strideAB * 8 <= kMaxBufferBytes &&
+           batch * strideP * 4 <= kMaxBufferBytes && batch * strideB * 8 <= kMaxBufferBytes &&
+           ldb * nrhs <= strideB;
+}
+
+bool window_fits(int64_t n, int64_t kl, int64_t ku, int64_t ldab) {
+    return ldab * n * 8 <= kMaxBufferBytes && n * 8 <= kMaxBufferBytes && kl <= 63 && kl + ku < 128;
+}
+
+int select_getrs(int64_t n, int64_t kl, int64_t ku, int64_t ldab, int64_t nrhs, int64_t strideAB,
+                 int64_t strideP, int64_t ldb, int64_t strideB, int64_t batch) {
+    const int64_t systems = batch * nrhs;
+    if (systems >= 64 && g16_fits(n, kl, ku, nrhs, strideAB, strideP, ldb, strideB, batch))
+        return BANDLU_GETRS_G16;
+    if (getrs_ring_fits(n, kl, ku, ldab)) return BANDLU_GETRS_RING;
+    if (window_fits(n, kl, ku, ldab)) return BANDLU_GETRS_WINDOW;
+    return BANDLU_GETRS_GENERIC;
+}
+
 int launch_getrs(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *dAB,
                  int64_t ldab, int64_t strideAB, const int32_t *d_ipiv, int64_t strideP,
-                 double *dB, int64_t ldb, int64_t strideB, int64_t batch, hipStream_t s) {
+                 double *dB, int64_t ldb, int64_t strideB, int64_t batch, int variant,
+                 hipStream_t s) {
     if (n == 0 || nrhs == 0 || batch == 0) return BANDLU_OK;
     RsParams P;
     P.AB = dAB;
@@ -469,23 +497,36 @@ int launch_getrs(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *
         set_error("band_getrs: batch * nrhs too large");
         return BANDLU_ERR_UNSUPPORTED;
     }
-    const bool buf_ok = ldab * n * 8 <= kMaxBufferBytes && n * 8 <= kMaxBufferBytes;
+    int v = variant;
+    if (v == 0) {
+        v = select_getrs(n, kl, ku, ldab, nrhs, strideAB, strideP, ldb, strideB, batch);
+    } else {
+        const bool ok = v == BANDLU_GETRS_G16 ? g16_fits(n, kl, ku, nrhs, strideAB, strideP, ldb, strideB, batch)
+                      : v == BANDLU_GETRS_RING ? getrs_ring_fits(n, kl, ku, ldab)
+                      : v == BANDLU_GETRS_WINDOW ? window_fits(n, kl, ku, ldab)
+                      : v == BANDLU_GETRS_GENERIC;
+        if (!ok) {
+            set_error("band_getrs: variant %d cannot solve n = %lld, kl = %lld, ku = %lld", v,
+                      (long long)n, (long long)kl, (long long)ku);
+            return BANDLU_ERR_UNSUPPORTED;
+        }
+    }
     // many systems with a small band: sixteen lanes per system
-    if (systems >= 64 && kl + ku <= 15 && batch * strideAB * 8 <= kMaxBufferBytes &&
-        batch * strideP * 4 <= kMaxBufferBytes && batch * strideB * 8 <= kMaxBufferBytes &&
-        ldb * nrhs <= strideB) {
+    if (v == BANDLU_GETRS_G16) {
         hipLaunchKernelGGL(getrs_g16_kernel, dim3((unsigned)((systems + 3) / 4)), dim3(64), 0, s, P,
                            systems);
         BANDLU_CHECK_LAUNCH("band_getrs (16 lanes per system)");
         return BANDLU_OK;
     }
-    if (buf_ok && kl <= 63 && kl + ku < 64) {
-        hipLaunchKernelGGL(getrs_win_kernel<1>, dim3((unsigned)systems), dim3(64), 0, s, P);
-        BANDLU_CHECK_LAUNCH("band_getrs (window)");
-        return BANDLU_OK;
-    }
-    if (buf_ok && kl <= 63 && kl + ku < 128) {
-        hipLaunchKernelGGL(getrs_win_kernel<2>, dim3((unsigned)systems), dim3(64), 0, s, P);
+    if (v == BANDLU_GETRS_RING)
+        return launch_getrs_ring(n, kl, ku, nrhs, dAB, ldab, strideAB, d_ipiv, strideP, dB, ldb,
+                                 strideB, batch, s);
+    if (v == BANDLU_GETRS_WINDOW) {
+        if (kl + ku < 64) {
+            hipLaunchKernelGGL(getrs_win_kernel<1>, dim3((unsigned)systems), dim3(64), 0, s, P);
+        } else {
+            hipLaunchKernelGGL(getrs_win_kernel<2>, dim3((unsigned)systems), dim3(64), 0, s, P);
+        }
         BANDLU_CHECK_LAUNCH("band_getrs (window)");
         return BANDLU_OK;
     }
@@ -523,7 +564,7 @@ extern "C" int band_getrs(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const
         set_error("band_getrs: n >= 2^31 is not supported");
         return BANDLU_ERR_UNSUPPORTED;
     }
-    return launch_getrs(n, kl, ku, nrhs, dAB, ldab, ldab * n, d_ipiv, n, dB, ldb, ldb * nrhs, 1,
+    return launch_getrs(n, kl, ku, nrhs, dAB, ldab, ldab * n, d_ipiv, n, dB, ldb, ldb * nrhs, 1, 0,
                         as_stream(stream));
 }
 
@@ -552,5 +593,45 @@ extern "C" int band_getrs_batched(int64_t n, int64_t kl, int64_t ku, int64_t nrh
         return BANDLU_ERR_UNSUPPORTED;
     }
     return launch_getrs(n, kl, ku, nrhs, dAB, ldab, strideAB, d_ipiv, strideP, dB, ldb, strideB,
-                        batch, as_stream(stream));
+                        batch, 0, as_stream(stream));
+}
+
+extern "C" int band_getrs_ex(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *dAB,
+                             int64_t ldab, int64_t strideAB, const int32_t *d_ipiv,
+                             int64_t strideP, double *dB, int64_t ldb, int64_t strideB,
+                             int64_t batch, int variant, void *stream) {
+    clear_error();
+    const int64_t bmax = n > 1 ? n - 1 : 0;
+    BANDLU_ARG(n >= 0, 1, "band_getrs_ex: n < 0");
+    BANDLU_ARG(kl >= 0 && kl <= bmax, 2, "band_getrs_ex: kl out of range");
+    BANDLU_ARG(ku >= 0 && ku <= bmax, 3, "band_getrs_ex: ku out of range");
+    BANDLU_ARG(nrhs >= 0, 4, "band_getrs_ex: nrhs < 0");
+    BANDLU_ARG(n == 0 || batch == 0 || dAB != nullptr, 5, "band_getrs_ex: dAB is null");
+    BANDLU_ARG(ldab >= 2 * kl + ku + 1, 6, "band_getrs_ex: ldab < 2kl+ku+1");
+    BANDLU_ARG(batch <= 1 || strideAB >= ldab * n, 7, "band_getrs_ex: strideAB < ldab*n");
+    BANDLU_ARG(n == 0 || batch == 0 || d_ipiv != nullptr, 8, "band_getrs_ex: d_ipiv is null");
+    BANDLU_ARG(batch <= 1 || strideP >= n, 9, "band_getrs_ex: strideP < n");
+    BANDLU_ARG(n == 0 || nrhs == 0 || batch == 0 || dB != nullptr, 10, "band_getrs_ex: dB is null");
+    BANDLU_ARG(ldb >= (n > 1 ? n : 1), 11, "band_getrs_ex: ldb < max(1, n)");
+    BANDLU_ARG(batch <= 1 || strideB >= ldb * nrhs, 12, "band_getrs_ex: strideB < ldb*nrhs");
+    BANDLU_ARG(batch >= 0, 13, "band_getrs_ex: batch < 0");
+    BANDLU_ARG(variant >= 0 && variant <= BANDLU_GETRS_GENERIC, 14, "band_getrs_ex: unknown variant");
+    if (n > kMaxN) {
+        set_error("band_getrs_ex: n >= 2^31 is not supported");
+        return BANDLU_ERR_UNSUPPORTED;
+    }
+    return launch_getrs(n, kl, ku, nrhs, dAB, ldab, strideAB, d_ipiv, strideP, dB, ldb, strideB,
+                        batch, variant, as_stream(stream));
+}
+
+extern "C" int band_getrs_variant(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, int64_t batch) {
+    const int64_t bmax = n > 1 ? n - 1 : 0;
+    if (n < 0) return -1;
+    if (kl < 0 || kl > bmax) return -2;
+    if (ku < 0 || ku > bmax) return -3;
+    if (nrhs < 0) return -4;
+    if (batch < 0) return -5;
+    const int64_t ldab = 2 * kl + ku + 1;
+    const int64_t ldb = n > 1 ? n : 1;
+    return select_getrs(n, kl, ku, ldab, nrhs, ldab * n, n, ldb, ldb * nrhs, batch);
 }

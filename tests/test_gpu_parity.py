@@ -311,6 +311,67 @@ def test_getrs_batched():
         assert_bitwise(got[b], xo, f"batch {b}")
 
 
+# Every solve kernel computes the same operations in the same order: each
+# must reproduce the oracle bit for bit wherever it applies.
+SOLVE_SHAPES = [(1, 0, 0), (2, 1, 0), (2, 0, 1), (3, 1, 1), (65, 64, 0), (70, 3, 66), (129, 10, 60),
+                (300, 63, 64), (500, 64, 63), (640, 127, 1), (700, 70, 100), (900, 128, 127),
+                (1000, 3, 3), (1200, 200, 300), (1500, 255, 300), (2000, 300, 700), (3000, 16, 16)]
+
+
+@pytest.mark.parametrize("n,kl,ku", SOLVE_SHAPES)
+def test_getrs_ring_exact(n, kl, ku):
+    rng = np.random.default_rng(n + 7 * kl + 13 * ku)
+    nrhs = 1 + (n % 3)
+    # pivoting inputs (no diagonal shift) as well as dominant ones
+    T = random_band(n, kl, ku, 1100 + n + kl, shift=0.0 if n % 2 else float(kl + ku))
+    _, ABo, ipo, _ = oracle_pipeline(T, kl, ku)
+    B = rng.standard_normal((nrhs, n))
+    xo = oracle.gbtrs(ABo, kl, ku, ipo, B.copy())
+    Bg = to_dev(B)
+    bandlu.band_getrs(to_dev(ABo), kl, ku, to_dev(ipo), Bg, variant="ring")
+    assert_bitwise(Bg.cpu().numpy(), xo, f"ring getrs n={n} kl={kl} ku={ku}")
+
+
+@pytest.mark.parametrize("n,kl,ku", [(1000, 3, 3), (300, 40, 20), (129, 10, 53), (90, 63, 0)])
+def test_getrs_window_exact(n, kl, ku):
+    T = random_band(n, kl, ku, 1300 + n, shift=0.0)
+    _, ABo, ipo, _ = oracle_pipeline(T, kl, ku)
+    B = np.random.default_rng(n).standard_normal((2, n))
+    xo = oracle.gbtrs(ABo, kl, ku, ipo, B.copy())
+    for variant in ("window", "generic"):
+        Bg = to_dev(B)
+        bandlu.band_getrs(to_dev(ABo), kl, ku, to_dev(ipo), Bg, variant=variant)
+        assert_bitwise(Bg.cpu().numpy(), xo, f"{variant} getrs n={n} kl={kl} ku={ku}")
+
+
+def test_getrs_ring_batched_and_padded():
+    batch, n, kl, ku, nrhs = 5, 400, 70, 90, 2
+    T = np.stack([random_band(n, kl, ku, 1400 + b) for b in range(batch)])
+    outs = [oracle_pipeline(T[b], kl, ku) for b in range(batch)]
+    AB = np.stack([o[1] for o in outs])
+    ip = np.stack([o[2] for o in outs])
+    ldb = n + 5  # padded right-hand sides: rows n..ldb-1 must stay untouched
+    B = np.random.default_rng(5).standard_normal((batch, nrhs, ldb))
+    Bg = to_dev(B)
+    bandlu.band_getrs_batched(to_dev(AB), kl, ku, to_dev(ip), Bg[:, :, :n], variant="ring")
+    got = Bg.cpu().numpy()
+    for b in range(batch):
+        xo = oracle.gbtrs(AB[b], kl, ku, ip[b], B[b, :, :n].copy())
+        assert_bitwise(got[b, :, :n], xo, f"batch {b}")
+    assert_bitwise(got[:, :, n:], B[:, :, n:], "padding", nan_payload=True)
+
+
+def test_getrs_ring_unsupported():
+    n, kl, ku = 2000, 500, 600  # kl + ku > 1023
+    AB = torch.zeros((n, 2 * kl + ku + 1), dtype=torch.float64, device=DEV)
+    ip = torch.ones(n, dtype=torch.int32, device=DEV)
+    with pytest.raises(bandlu.BandLUError):
+        bandlu.band_getrs(AB, kl, ku, ip, torch.zeros((1, n), dtype=torch.float64, device=DEV),
+                          variant="ring")
+    assert bandlu.band_getrs_variant(32768, 256, 256) == "ring"
+    assert bandlu.band_getrs_variant(256, 4, 4, 1, 4096) == "g16"
+
+
 # ----------------------------------------------------------- blocked getrf --
 BLOCKED_SHAPES = [(300, 40, 3), (95, 20, 52), (700, 100, 150), (1100, 256, 256), (530, 33, 200),
                   (64, 63, 63), (257, 32, 0), (400, 250, 1), (300, 31, 90), (97, 12, 80)]
