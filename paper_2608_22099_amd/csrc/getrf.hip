@@ -4,6 +4,9 @@
 // Variants (band_getrf_variant):
 //   WINDOW      kl <= 31 and 2kl+ku+1 <= 64, or kl <= 15 and 2kl+ku+1 <= 128:
 //               register window, 64 lanes per matrix (getrf_win64.hpp);
+//   SPLIT       1 <= kl <= 31 with the WINDOW limits: the window plus a
+//               second wavefront that runs the pivot decisions
+//               (getrf_split.hpp);
 //   WINDOW_G16  batched, kl <= 7 and 2kl+ku+1 <= 32: register window, 16
 //               lanes per matrix, four matrices per wavefront;
 //   BLOCKED     kl <= 31 beyond the windows: panels of 32 columns factored in
@@ -32,6 +35,15 @@ WinKernel win_kernel_g64_c2_h1_8(int H);
 WinKernel win_kernel_g64_c2_h9_16(int H);
 WinKernel win_kernel_g16_c1_h1_8(int H);
 WinKernel win_kernel_g16_c2_h1_8(int H);
+WinKernel split_kernel_c1_h2_16(int H);
+WinKernel split_kernel_c1_h17_32(int H);
+WinKernel split_kernel_c2_h2_16(int H);
+
+// two-wavefront kernel (getrf_split.hpp) for 2 <= H <= 32
+WinKernel split_kernel(int CPL, int H) {
+    if (CPL == 1) return H <= 16 ? split_kernel_c1_h2_16(H) : split_kernel_c1_h17_32(H);
+    return split_kernel_c2_h2_16(H);
+}
 
 WinKernel win_kernel(int G, int CPL, int H) {
     if (G == 16) {
@@ -172,6 +184,9 @@ __global__ void zero_info_kernel(int32_t *info, int64_t batch) {
 int select_variant(int64_t n, int64_t kl, int64_t ku, int64_t batch) {
     const int64_t need = 2 * kl + ku + 1;
     if (batch >= 64 && kl <= 7 && need <= 32) return BANDLU_GETRF_WINDOW_G16;
+    if (kl >= 1 && kl <= 31 && (need <= 64 || (need <= 128 && kl <= 15)) &&
+        need * n * 8 <= kMaxBufferBytes)
+        return BANDLU_GETRF_SPLIT;
     if (kl <= 31 && (need <= 64 || (need <= 128 && kl <= 15)) && need * n * 8 <= kMaxBufferBytes)
         return BANDLU_GETRF_WINDOW;
     // from kl = 32 on, applying a panel of 32 columns is a real dense product
@@ -191,6 +206,9 @@ bool variant_fits(int v, int64_t n, int64_t kl, int64_t ku, int64_t ldab, int64_
         return kl <= 7 && need <= 32 && ldab * n * 8 <= kMaxBufferBytes;
     case BANDLU_GETRF_WINDOW:
         return kl <= 31 && (need <= 64 || (need <= 128 && kl <= 15)) &&
+               ldab * n * 8 <= kMaxBufferBytes;
+    case BANDLU_GETRF_SPLIT:
+        return kl >= 1 && kl <= 31 && (need <= 64 || (need <= 128 && kl <= 15)) &&
                ldab * n * 8 <= kMaxBufferBytes;
     case BANDLU_GETRF_BLOCKED:
     case BANDLU_GETRF_BLOCKED_MFMA:
@@ -254,6 +272,26 @@ int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
         const int64_t blocks = (batch + per_wave - 1) / per_wave;
         hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(64), 0, s, W);
         BANDLU_CHECK_LAUNCH("band_getrf (window)");
+        return BANDLU_OK;
+    }
+    if (v == BANDLU_GETRF_SPLIT) {
+        WinParams W;
+        W.AB = dAB;
+        W.ipiv = d_ipiv;
+        W.info = d_info;
+        W.ldab = ldab;
+        W.strideAB = strideAB;
+        W.strideP = strideP;
+        W.n = (int)n;
+        W.ku = (int)ku;
+        W.batch = (int)batch;
+        const WinKernel k = split_kernel(need <= 64 ? 1 : 2, (int)kl + 1);
+        if (!k) {
+            set_error("band_getrf: no two-wavefront kernel for kl = %lld", (long long)kl);
+            return BANDLU_ERR_UNSUPPORTED;
+        }
+        hipLaunchKernelGGL(k, dim3((unsigned)batch), dim3(128), 0, s, W);
+        BANDLU_CHECK_LAUNCH("band_getrf (two wavefronts)");
         return BANDLU_OK;
     }
     if (v == BANDLU_GETRF_BLOCKED)
@@ -346,7 +384,7 @@ extern "C" int band_getrf_ex(int64_t n, int64_t kl, int64_t ku, double *dAB, int
     BANDLU_ARG(batch <= 1 || strideP >= n, 8, "band_getrf_ex: strideP < n");
     BANDLU_ARG(batch == 0 || d_info != nullptr, 9, "band_getrf_ex: d_info is null");
     BANDLU_ARG(batch >= 0, 10, "band_getrf_ex: batch < 0");
-    BANDLU_ARG(variant >= 0 && variant <= BANDLU_GETRF_BLOCKED_MFMA, 11,
+    BANDLU_ARG(variant >= 0 && variant <= BANDLU_GETRF_SPLIT, 11,
                "band_getrf_ex: unknown variant");
     if (n > kMaxN || batch > INT_MAX) {
         set_error("band_getrf_ex: sizes too large");

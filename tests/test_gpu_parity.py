@@ -187,6 +187,49 @@ def test_getrf_window_boundaries(kl, ku):
         assert_bitwise(g[1], o[1], f"n={n} kl={kl} ku={ku}")
 
 
+# The two-wavefront kernel and the one-wavefront window run the same
+# operations: both must reproduce the oracle bit for bit, with and without
+# row interchanges (no diagonal shift: interchanges at most steps).
+SPLIT_SHAPES = [(2, 1, 0), (2, 1, 1), (3, 2, 0), (40, 1, 0), (50, 3, 2), (300, 3, 3), (300, 16, 16),
+                (257, 31, 1), (65, 30, 3), (200, 2, 64), (300, 15, 97), (130, 8, 50), (1000, 5, 5),
+                (129, 7, 0), (64, 1, 62)]
+
+
+@pytest.mark.parametrize("n,kl,ku", SPLIT_SHAPES)
+def test_getrf_split_exact(n, kl, ku):
+    for shift in (0.0, float(kl + ku)):
+        T = random_band(n, kl, ku, 31 + n + kl, shift=shift)
+        o = oracle_pipeline(T, kl, ku)
+        for variant in ("split", "window"):
+            g = gpu_pipeline(T, kl, ku, variant=variant)
+            what = f"{variant} n={n} kl={kl} ku={ku} shift={shift}"
+            assert np.array_equal(g[2], o[2]), what
+            assert g[3] == o[3], what
+            assert_bitwise(g[1], o[1], what)
+
+
+def test_getrf_split_special():
+    """Singular columns, NaN entries, pivots below DBL_MIN and a zero matrix
+    through the two-wavefront kernel."""
+    n, kl, ku = 60, 3, 2
+    cases = []
+    for k in (0, 7, 59):
+        T = random_band(n, kl, ku, 5 + k)
+        T[k, :] = 0.0
+        cases.append(("singular", T, kl, ku))
+    T = random_band(n, kl, ku, 99)
+    T[4, 4] = np.nan
+    T[10, 12] = np.nan
+    cases.append(("nan", T, kl, ku))
+    cases.append(("tiny", random_band(n, 2, 2, 5) * 1e-300, 2, 2))
+    cases.append(("zero", np.zeros((20, 20)), 2, 3))
+    for what, T, a, c in cases:
+        g = gpu_pipeline(T, a, c, variant="split")
+        o = oracle_pipeline(T, a, c)
+        assert np.array_equal(g[2], o[2]) and g[3] == o[3], what
+        assert_bitwise(g[1], o[1], what)
+
+
 def test_getrf_singular_and_nan():
     n, kl, ku = 50, 3, 2
     for k in [0, 7, 49]:
