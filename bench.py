@@ -50,9 +50,12 @@ STEP_SOURCES = {
     "detect": ["detect.hip", "common.hpp"],
     "convert": ["convert.hip", "common.hpp"],
     "getrf": ["getrf.hip", "getrf_win64.hpp", "getrf_win2.hpp", "getrf_window.hpp", "getrf_g16.hpp",
-              "getrf_blocked.hip", "getrf_mfma.hip", "wave.hpp", "bufio.hpp", "common.hpp"],
-    "getrs": ["getrs.hip", "bufio.hpp", "common.hpp"],
+              "getrf_split.hpp", "getrf_blocked.hip", "getrf_mfma.hip", "wave.hpp", "bufio.hpp",
+              "common.hpp"],
+    "getrs": ["getrs.hip", "getrs_ring.hpp", "getrs_ring.hip", "bufio.hpp", "common.hpp"],
 }
+# instantiation files of a step (one per parameter range), by name prefix
+STEP_PREFIXES = {"getrf": ("getrf_win_g", "getrf_split_c"), "getrs": ("getrs_ring_fwd", "getrs_ring_bwd")}
 
 
 def source_hash(step):
@@ -60,8 +63,8 @@ def source_hash(step):
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2608_22099_amd", "csrc")
     files = list(STEP_SOURCES[step])
-    if step == "getrf":
-        files += sorted(f for f in os.listdir(csrc) if f.startswith("getrf_win_g"))
+    for prefix in STEP_PREFIXES.get(step, ()):
+        files += sorted(f for f in os.listdir(csrc) if f.startswith(prefix))
     for f in files:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + b"\0" + fh.read())
