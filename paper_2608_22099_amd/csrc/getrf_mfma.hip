@@ -206,21 +206,91 @@ __global__ __launch_bounds__(kThreads) void mfma_step_kernel(MfmaParams P) {
     const int xr = NB + t;  // row of band row jn+t in the block above
     const bool from_lds = upd && xr < R;
     double x[NB];
-    unsigned okx = 0, okl = 0;
+    auto load_panel = [&]() __attribute__((always_inline)) {
+        unsigned okx = 0, okl = 0;
 #pragma unroll
-    for (int c = 0; c < NB; ++c) {
-        const int d = t - c;
-        const bool inb = own & (c < nbn) & (d >= -kv) & (d <= kl);
-        const bool lds = inb & from_lds & (c < W);
-        okx |= unsigned(inb & !lds) << c;
-        okl |= unsigned(lds) << c;
-        x[c] = ld_clamped(AB, int64_t(jn + c) * ldab + (kv + d), inb & !lds);
-    }
+        for (int c = 0; c < NB; ++c) {
+            const int d = t - c;
+            const bool inb = own & (c < nbn) & (d >= -kv) & (d <= kl);
+            const bool lds = inb & from_lds & (c < W);
+            okx |= unsigned(inb & !lds) << c;
+            okl |= unsigned(lds) << c;
+            x[c] = ld_clamped(AB, int64_t(jn + c) * ldab + (kv + d), inb & !lds);
+        }
 #pragma unroll
-    for (int c = 0; c < NB; ++c) {
-        const double l = sX[min(xr, kRows - 1) * LDX + c];
-        x[c] = (okl >> c & 1u) ? l : keep_if(x[c], okx, c);
+        for (int c = 0; c < NB; ++c) {
+            const double l = sX[min(xr, kRows - 1) * LDX + c];
+            x[c] = (okl >> c & 1u) ? l : keep_if(x[c], okx, c);
+        }
+    };
+    load_panel();
+
+    // ---- first attempt: the panel with every pivot on the diagonal.  Partial
+    // pivoting keeps the diagonal entry exactly when no candidate below it has
+    // a larger pivot key (a tie goes to the first, the diagonal), so each
+    // thread checks its row at every step; the pivot row is then known before
+    // the column is reduced, and one thread publishes it for the next step
+    // while the others update.  The operations are those of the pivoting loop
+    // below whenever it would not interchange, so the results are the same.
+    // Nothing is written before the whole panel has passed; on the first
+    // column whose diagonal would not be chosen, the panel is loaded again and
+    // factored by the pivoting loop.
+    __shared__ double sP[2][NB];  // row jn+q as it stands at step q
+    __shared__ int s_viol[2];     // a row ranked above the diagonal at step q (by parity)
+    bool verified = false;
+    if (t == 0) {
+#pragma unroll
+        for (int c = 0; c < NB; ++c) sP[0][c] = x[c];
+        s_viol[0] = s_viol[1] = 0;
     }
+    lds_barrier();
+    {
+        int finfo = 0;
+        bool ok = true;
+#pragma unroll
+        for (int q = 0; q < NB; ++q) {
+            if (q < nbn) {
+                const int par = q & 1;
+                const double piv = sP[par][q];
+                const int km = min(kl, n - 1 - (jn + q));
+                const int tt = t - q;
+                const bool cand = own & (tt >= 1) & (tt <= km);
+                if (__ballot(cand && pivot_key(x[q], tt) > pivot_key(piv, 0)) && lane == 0) s_viol[par] = 1;
+                if (piv != 0.0) {
+                    if (cand) {
+                        const double l = fabs(piv) >= DBL_MIN ? x[q] * (1.0 / piv) : x[q] / piv;
+                        x[q] = l;
+#pragma unroll
+                        for (int c = q + 1; c < NB; ++c) x[c] = __builtin_fma(-l, sP[par][c], x[c]);
+                    }
+                } else if (finfo == 0) {
+                    finfo = jn + q + 1;
+                }
+                if (t == q + 1) {
+#pragma unroll
+                    for (int c = q + 1; c < NB; ++c) sP[par ^ 1][c] = x[c];
+                }
+                lds_barrier();
+                if (s_viol[par]) {
+                    ok = false;
+                    break;
+                }
+            }
+        }
+        if (ok) {
+            // no interchange: pivots, multipliers and U entries stay in place
+            if (t < nbn) ipiv[jn + t] = jn + t + 1;
+#pragma unroll
+            for (int c = 0; c < NB; ++c) {
+                const int d = t - c;
+                if (own && c < nbn && d >= -kv && d <= kl) AB[int64_t(jn + c) * ldab + (kv + d)] = x[c];
+            }
+            if (t == 0 && finfo != 0 && P.info[bm] == 0) P.info[bm] = finfo;
+            verified = true;
+        }
+    }
+    if (verified) return;
+    load_panel();
     int myrow = t;
     int info = 0;
 #pragma unroll 1

@@ -502,6 +502,61 @@ def test_getrf_mfma_pivoting_and_singular():
     assert g[3] == 1
 
 
+@pytest.mark.parametrize("n,kl,ku", [(300, 40, 3), (1100, 256, 256), (257, 32, 0), (65, 40, 24),
+                                     (600, 256, 343), (97, 96, 5)])
+def test_getrf_mfma_no_interchange(n, kl, ku):
+    """Diagonally dominant bands: every panel keeps its diagonal pivots, so
+    the kernel's no-interchange attempt passes on every panel."""
+    T = random_band(n, kl, ku, 17 * n + kl, shift=4.0 * (kl + 1))
+    g, o = check_mfma(T, kl, ku, f"dominant n={n} kl={kl} ku={ku}")
+    assert np.array_equal(o[2], np.arange(1, n + 1))
+
+
+@pytest.mark.parametrize("col", [0, 1, 30, 31, 32, 63, 64, 95, 190, 191])
+def test_getrf_mfma_late_interchange(col):
+    """A dominant band with one weak diagonal: the no-interchange attempt runs
+    up to that column of its panel, then the panel is factored again with
+    pivoting; panels before and after pass."""
+    n, kl, ku = 192, 48, 20
+    T = random_band(n, kl, ku, 900 + col, shift=4.0 * (kl + 1))
+    T[col, col] = 1e-3  # T[j, i] is A[i, j]
+    g, o = check_mfma(T, kl, ku, f"weak diagonal {col}")
+    assert o[2][col] != col + 1 or col == n - 1
+
+
+def test_getrf_mfma_no_interchange_ties_and_zeros():
+    """Cases decided without an interchange: a candidate equal in magnitude
+    to the diagonal (the diagonal wins the tie), and a zero column in a
+    dominant band (zero pivot, info set, factorisation goes on)."""
+    n, kl, ku = 200, 40, 10
+    T = random_band(n, kl, ku, 77, shift=4.0 * (kl + 1))
+    T[0, 1] = -T[0, 0]  # A[1, 0] = -A[0, 0]
+    T[0, 5] = T[0, 0]
+    g, o = check_mfma(T, kl, ku, "tie in the first column")
+    assert o[2][0] == 1
+    for col in (0, 33, 63, 199):
+        S = random_band(n, kl, ku, 78 + col, shift=4.0 * (kl + 1))
+        S[col, :] = 0.0
+        g, o = check_mfma(S, kl, ku, f"zero column {col} in a dominant band")
+        assert o[3] == col + 1
+
+
+def test_getrf_mfma_no_interchange_batched():
+    """A batch mixing dominant systems (no interchange) with ones that pivot."""
+    batch, n, kl, ku = 5, 230, 48, 40
+    T = np.stack([random_band(n, kl, ku, 310 + b, shift=(4.0 * (kl + 1) if b % 2 == 0 else 0.0))
+                  for b in range(batch)])
+    AB = bandlu.dense_to_band_batched(to_dev(T), kl, ku)
+    AB0 = AB.cpu().numpy()
+    ipiv, info = bandlu.band_getrf_batched(AB, kl, ku)
+    ABg, ipg, infg = AB.cpu().numpy(), ipiv.cpu().numpy(), info.cpu().numpy()
+    for b in range(batch):
+        o = oracle_pipeline(T[b], kl, ku)
+        assert np.array_equal(ipg[b], o[2]) and infg[b] == o[3], b
+        assert_factors_close(ABg[b], o[1], kl, ku, f"batch {b}")
+        assert_backward_error(AB0[b], ABg[b], kl, ku, ipg[b], f"batch {b}")
+
+
 def test_getrf_mfma_batched():
     batch, n, kl, ku = 6, 230, 48, 40
     T = np.stack([random_band(n, kl, ku, 300 + b) for b in range(batch)])
