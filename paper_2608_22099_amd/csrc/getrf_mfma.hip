@@ -27,6 +27,7 @@
 #include <algorithm>
 #include <cfloat>
 #include <climits>
+#include <utility>
 
 #include "common.hpp"
 #include "wave.hpp"
@@ -206,7 +207,17 @@ __global__ __launch_bounds__(kThreads) void mfma_step_kernel(MfmaParams P) {
     const int xr = NB + t;  // row of band row jn+t in the block above
     const bool from_lds = upd && xr < R;
     double x[NB];
+    // band entry (row jn+t, column jn+c) is at diag0 + c * (ldab - 1); the
+    // stride is hidden from the optimiser where it is used, so that the 32
+    // column offsets are formed there and not kept live across the kernel
+    const int64_t diag0 = int64_t(jn) * ldab + kv + t;
+    auto colstep = [&]() __attribute__((always_inline)) {
+        int64_t st = ldab - 1;
+        asm volatile("" : "+s"(st));
+        return st;
+    };
     auto load_panel = [&]() __attribute__((always_inline)) {
+        const int64_t st = colstep();
         unsigned okx = 0, okl = 0;
 #pragma unroll
         for (int c = 0; c < NB; ++c) {
@@ -215,7 +226,7 @@ __global__ __launch_bounds__(kThreads) void mfma_step_kernel(MfmaParams P) {
             const bool lds = inb & from_lds & (c < W);
             okx |= unsigned(inb & !lds) << c;
             okl |= unsigned(lds) << c;
-            x[c] = ld_clamped(AB, int64_t(jn + c) * ldab + (kv + d), inb & !lds);
+            x[c] = ld_clamped(AB, diag0 + c * st, inb & !lds);
         }
 #pragma unroll
         for (int c = 0; c < NB; ++c) {
@@ -227,67 +238,128 @@ __global__ __launch_bounds__(kThreads) void mfma_step_kernel(MfmaParams P) {
 
     // ---- first attempt: the panel with every pivot on the diagonal.  Partial
     // pivoting keeps the diagonal entry exactly when no candidate below it has
-    // a larger pivot key (a tie goes to the first, the diagonal), so each
-    // thread checks its row at every step; the pivot row is then known before
-    // the column is reduced, and one thread publishes it for the next step
-    // while the others update.  The operations are those of the pivoting loop
-    // below whenever it would not interchange, so the results are the same.
-    // Nothing is written before the whole panel has passed; on the first
-    // column whose diagonal would not be chosen, the panel is loaded again and
-    // factored by the pivoting loop.
-    __shared__ double sP[2][NB];  // row jn+q as it stands at step q
-    __shared__ int s_viol[2];     // a row ranked above the diagonal at step q (by parity)
-    bool verified = false;
-    if (t == 0) {
+    // a larger pivot key (a tie goes to the first, the diagonal), so every
+    // thread checks its row at every step instead of taking part in an argmax.
+    // Without interchanges row s is final once steps 0..s-1 have reached it,
+    // and the rows below need nothing but the pivot rows: wave 0 (rows 0..63)
+    // runs the 32 steps, taking pivot row s from lane s with lane reads, and
+    // publishes the pivot rows in groups of eight; the other waves apply each
+    // group while wave 0 computes the next one.  Every entry gets its updates
+    // in the order of the steps, with the operations of the pivoting loop
+    // below, so the results are those of that loop whenever it would not
+    // interchange.  Nothing is written before the whole panel has passed; if
+    // any row outranks its diagonal, the panel is loaded again and factored by
+    // the pivoting loop.
+    constexpr int LDU = NB + 2;  // pivot row s: sU[s * LDU + c], c >= s; its reciprocal at c = NB
+    double *const sU = sLT;      // (the applied panel's L is no longer needed)
+    __shared__ int s_viol;
+    bool viol = false;
+    int finfo = 0;
+    if (t == 0) s_viol = 0;
+    const int ngrp = (nbn + 7) / 8;
+    double r = 1.0 / x[0];  // wave 0: reciprocal of this row's entry in the next step's column
+    double myrcp = 0.0;     // wave 0, lane s: the reciprocal of its pivot, once step s has run
+    // step S in wave 0: pivot row S is lane S's row
+    auto step_w0 = [&]<int S>() __attribute__((always_inline)) {
+        if (S >= nbn) return;
+        const double piv = readlane_d(x[S], S);
+        const double rcp = readlane_d(r, S);
+        myrcp = lane == S ? rcp : myrcp;
+        const int km = min(kl, n - 1 - (jn + S));
+        const int tt = t - S;
+        const bool cand = own & (tt >= 1) & (tt <= km);
+        viol |= cand && pivot_key(x[S], tt) > pivot_key(piv, 0);
+        double u[NB];
 #pragma unroll
-        for (int c = 0; c < NB; ++c) sP[0][c] = x[c];
-        s_viol[0] = s_viol[1] = 0;
+        for (int c = S + 1; c < NB; ++c) u[c] = readlane_d(x[c], S);
+        if (piv != 0.0) {
+            double l;
+            if (fabs(piv) >= DBL_MIN) {
+                l = x[S] * rcp;
+            } else {
+                l = x[S] / piv;
+            }
+            if (cand) {
+                x[S] = l;
+#pragma unroll
+                for (int c = S + 1; c < NB; ++c) x[c] = __builtin_fma(-l, u[c], x[c]);
+            }
+        } else if (finfo == 0) {
+            finfo = jn + S + 1;
+        }
+        if constexpr (S + 1 < NB) r = 1.0 / x[S + 1];
+    };
+    // step S in the other waves: pivot row S from LDS
+    auto step_wk = [&]<int S>() __attribute__((always_inline)) {
+        if (S >= nbn) return;
+        const double *us = sU + S * LDU;
+        const double piv = us[S];
+        const int km = min(kl, n - 1 - (jn + S));
+        const int tt = t - S;
+        const bool cand = own & (tt >= 1) & (tt <= km);
+        viol |= cand && pivot_key(x[S], tt) > pivot_key(piv, 0);
+        if (piv != 0.0) {
+            double l;
+            if (fabs(piv) >= DBL_MIN) {
+                l = x[S] * us[NB];
+            } else {
+                l = x[S] / piv;
+            }
+            if (cand) {
+                x[S] = l;
+#pragma unroll
+                for (int c = S + 1; c < NB; ++c) x[c] = __builtin_fma(-l, us[c], x[c]);
+            }
+        } else if (finfo == 0) {
+            finfo = jn + S + 1;
+        }
+    };
+    auto group_w0 = [&]<int G>() __attribute__((always_inline)) {
+        if (G >= ngrp) return;
+        [&]<int... Q>(std::integer_sequence<int, Q...>) __attribute__((always_inline)) {
+            (step_w0.template operator()<8 * G + Q>(), ...);
+        }(std::make_integer_sequence<int, 8>{});
+        // rows 8G..8G+7 are final: publish them with their reciprocals
+        if (lane >= 8 * G && lane < 8 * G + 8) {
+#pragma unroll
+            for (int c = 8 * G; c < NB; ++c) sU[lane * LDU + c] = x[c];
+            sU[lane * LDU + NB] = myrcp;
+        }
+        lds_barrier();
+    };
+    auto group_wk = [&]<int G>() __attribute__((always_inline)) {
+        if (G >= ngrp) return;
+        lds_barrier();
+        [&]<int... Q>(std::integer_sequence<int, Q...>) __attribute__((always_inline)) {
+            (step_wk.template operator()<8 * G + Q>(), ...);
+        }(std::make_integer_sequence<int, 8>{});
+    };
+    static_assert(NB == 32, "four groups of eight steps");
+    if (__builtin_amdgcn_readfirstlane(wv) == 0) {  // (uniform, so each wave sees only its own barriers)
+        group_w0.template operator()<0>();
+        group_w0.template operator()<1>();
+        group_w0.template operator()<2>();
+        group_w0.template operator()<3>();
+    } else {
+        group_wk.template operator()<0>();
+        group_wk.template operator()<1>();
+        group_wk.template operator()<2>();
+        group_wk.template operator()<3>();
     }
+    if (__ballot(viol) && lane == 0) s_viol = 1;
     lds_barrier();
-    {
-        int finfo = 0;
-        bool ok = true;
+    bool verified = false;
+    if (s_viol == 0) {
+        // no interchange: pivots, multipliers and U entries stay in place
+        if (t < nbn) ipiv[jn + t] = jn + t + 1;
+        const int64_t st = colstep();
 #pragma unroll
-        for (int q = 0; q < NB; ++q) {
-            if (q < nbn) {
-                const int par = q & 1;
-                const double piv = sP[par][q];
-                const int km = min(kl, n - 1 - (jn + q));
-                const int tt = t - q;
-                const bool cand = own & (tt >= 1) & (tt <= km);
-                if (__ballot(cand && pivot_key(x[q], tt) > pivot_key(piv, 0)) && lane == 0) s_viol[par] = 1;
-                if (piv != 0.0) {
-                    if (cand) {
-                        const double l = fabs(piv) >= DBL_MIN ? x[q] * (1.0 / piv) : x[q] / piv;
-                        x[q] = l;
-#pragma unroll
-                        for (int c = q + 1; c < NB; ++c) x[c] = __builtin_fma(-l, sP[par][c], x[c]);
-                    }
-                } else if (finfo == 0) {
-                    finfo = jn + q + 1;
-                }
-                if (t == q + 1) {
-#pragma unroll
-                    for (int c = q + 1; c < NB; ++c) sP[par ^ 1][c] = x[c];
-                }
-                lds_barrier();
-                if (s_viol[par]) {
-                    ok = false;
-                    break;
-                }
-            }
+        for (int c = 0; c < NB; ++c) {
+            const int d = t - c;
+            if (own && c < nbn && d >= -kv && d <= kl) AB[diag0 + c * st] = x[c];
         }
-        if (ok) {
-            // no interchange: pivots, multipliers and U entries stay in place
-            if (t < nbn) ipiv[jn + t] = jn + t + 1;
-#pragma unroll
-            for (int c = 0; c < NB; ++c) {
-                const int d = t - c;
-                if (own && c < nbn && d >= -kv && d <= kl) AB[int64_t(jn + c) * ldab + (kv + d)] = x[c];
-            }
-            if (t == 0 && finfo != 0 && P.info[bm] == 0) P.info[bm] = finfo;
-            verified = true;
-        }
+        if (t == 0 && finfo != 0 && P.info[bm] == 0) P.info[bm] = finfo;
+        verified = true;
     }
     if (verified) return;
     load_panel();
