@@ -178,11 +178,13 @@ int band_getrs_batched(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const do
 #define BANDLU_GETRF_BLOCKED 4      /* blocked, exact rank-1 trailing updates   */
 #define BANDLU_GETRF_BLOCKED_MFMA 5 /* blocked, fp64 MFMA trailing update       */
 #define BANDLU_GETRF_SPLIT 6        /* register window + a pivot wavefront      */
+#define BANDLU_GETRF_DIAG 7         /* diagonal pivots verified per column, the */
+                                    /* split kernel from the first failing one  */
 int band_getrf_variant(int64_t n, int64_t kl, int64_t ku, int64_t batch);
 
 /*
  * band_getrf_ex -- band_getrf_batched with the kernel chosen by the caller:
- * variant 0 picks it as band_getrf_batched does, 1..6 forces that
+ * variant 0 picks it as band_getrf_batched does, 1..7 forces that
  * BANDLU_GETRF_* kernel.  Arguments 1-10 as in band_getrf_batched (argument
  * 11 is the variant).  A variant that cannot handle the sizes (a window for
  * kl > 31 or a band wider than its registers, a blocked variant for

@@ -4,6 +4,11 @@
 // Variants (band_getrf_variant):
 //   WINDOW      kl <= 31 and 2kl+ku+1 <= 64, or kl <= 15 and 2kl+ku+1 <= 128:
 //               register window, 64 lanes per matrix (getrf_win64.hpp);
+//   DIAG        1 <= kl, 1 <= ku <= 24, ldab <= 64 and kl small enough
+//               for one lane per live row: every column is first factored
+//               with its diagonal pivot and checked against partial pivoting
+//               (getrf_diag.hpp); from the first column that fails, SPLIT
+//               factors the rest;
 //   SPLIT       1 <= kl <= 31 with the WINDOW limits: the window plus a
 //               second wavefront that runs the pivot decisions
 //               (getrf_split.hpp);
@@ -23,6 +28,7 @@
 #include <climits>
 
 #include "bufio.hpp"
+#include "getrf_diag.hpp"
 #include "getrf_window.hpp"
 
 namespace bandlu {
@@ -43,6 +49,19 @@ WinKernel split_kernel_c2_h2_16(int H);
 WinKernel split_kernel(int CPL, int H) {
     if (CPL == 1) return H <= 16 ? split_kernel_c1_h2_16(H) : split_kernel_c1_h17_32(H);
     return split_kernel_c2_h2_16(H);
+}
+
+// diagonal-pivot kernel (getrf_diag.hpp) for 1 <= ku <= kDiagMaxKu
+WinKernel diag_kernel(int KU) {
+    if (KU >= 1 && KU <= 8) return diag_kernel_ku1_8(KU);
+    if (KU >= 9 && KU <= 16) return diag_kernel_ku9_16(KU);
+    if (KU >= 17 && KU <= 24) return diag_kernel_ku17_24(KU);
+    return nullptr;
+}
+
+bool diag_fits(int64_t n, int64_t kl, int64_t ku, int64_t ldab) {
+    return kl >= 1 && ku >= 1 && ku <= kDiagMaxKu && kl <= diag_max_kl((int)ku) &&
+           2 * kl + ku + 1 <= 64 && ldab <= 64 && n >= 2 && ldab * n * 8 <= kMaxBufferBytes;
 }
 
 WinKernel win_kernel(int G, int CPL, int H) {
@@ -184,6 +203,7 @@ __global__ void zero_info_kernel(int32_t *info, int64_t batch) {
 int select_variant(int64_t n, int64_t kl, int64_t ku, int64_t batch) {
     const int64_t need = 2 * kl + ku + 1;
     if (batch >= 64 && kl <= 7 && need <= 32) return BANDLU_GETRF_WINDOW_G16;
+    if (diag_fits(n, kl, ku, need)) return BANDLU_GETRF_DIAG;
     if (kl >= 1 && kl <= 31 && (need <= 64 || (need <= 128 && kl <= 15)) &&
         need * n * 8 <= kMaxBufferBytes)
         return BANDLU_GETRF_SPLIT;
@@ -210,6 +230,8 @@ bool variant_fits(int v, int64_t n, int64_t kl, int64_t ku, int64_t ldab, int64_
     case BANDLU_GETRF_SPLIT:
         return kl >= 1 && kl <= 31 && (need <= 64 || (need <= 128 && kl <= 15)) &&
                ldab * n * 8 <= kMaxBufferBytes;
+    case BANDLU_GETRF_DIAG:
+        return diag_fits(n, kl, ku, ldab);
     case BANDLU_GETRF_BLOCKED:
     case BANDLU_GETRF_BLOCKED_MFMA:
         return kl <= 256 && batch <= 65535;
@@ -251,6 +273,8 @@ int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
         W.n = (int)n;
         W.ku = (int)ku;
         W.batch = (int)batch;
+        W.kl = (int)kl;
+        W.resume = 0;
         const int H = (int)kl + 1;
         WinKernel k;
         int per_wave;
@@ -285,6 +309,8 @@ int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
         W.n = (int)n;
         W.ku = (int)ku;
         W.batch = (int)batch;
+        W.kl = (int)kl;
+        W.resume = 0;
         const WinKernel k = split_kernel(need <= 64 ? 1 : 2, (int)kl + 1);
         if (!k) {
             set_error("band_getrf: no two-wavefront kernel for kl = %lld", (long long)kl);
@@ -292,6 +318,35 @@ int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
         }
         hipLaunchKernelGGL(k, dim3((unsigned)batch), dim3(128), 0, s, W);
         BANDLU_CHECK_LAUNCH("band_getrf (two wavefronts)");
+        return BANDLU_OK;
+    }
+    if (v == BANDLU_GETRF_DIAG) {
+        WinParams W;
+        W.AB = dAB;
+        W.ipiv = d_ipiv;
+        W.info = d_info;
+        W.ldab = ldab;
+        W.strideAB = strideAB;
+        W.strideP = strideP;
+        W.n = (int)n;
+        W.ku = (int)ku;
+        W.batch = (int)batch;
+        W.kl = (int)kl;
+        W.resume = 0;
+        const WinKernel k = diag_kernel((int)ku);
+        const WinKernel rest = split_kernel(1, (int)kl + 1);
+        if (!k || !rest) {
+            set_error("band_getrf: no diagonal-pivot kernel for kl = %lld, ku = %lld", (long long)kl,
+                      (long long)ku);
+            return BANDLU_ERR_UNSUPPORTED;
+        }
+        hipLaunchKernelGGL(k, dim3((unsigned)batch), dim3(64), 0, s, W);
+        BANDLU_CHECK_LAUNCH("band_getrf (diagonal pivots)");
+        // columns from the first failing one on (a launch that returns at
+        // once where every column passed)
+        W.resume = 1;
+        hipLaunchKernelGGL(rest, dim3((unsigned)batch), dim3(128), 0, s, W);
+        BANDLU_CHECK_LAUNCH("band_getrf (two wavefronts, resumed)");
         return BANDLU_OK;
     }
     if (v == BANDLU_GETRF_BLOCKED)
@@ -384,7 +439,7 @@ extern "C" int band_getrf_ex(int64_t n, int64_t kl, int64_t ku, double *dAB, int
     BANDLU_ARG(batch <= 1 || strideP >= n, 8, "band_getrf_ex: strideP < n");
     BANDLU_ARG(batch == 0 || d_info != nullptr, 9, "band_getrf_ex: d_info is null");
     BANDLU_ARG(batch >= 0, 10, "band_getrf_ex: batch < 0");
-    BANDLU_ARG(variant >= 0 && variant <= BANDLU_GETRF_SPLIT, 11,
+    BANDLU_ARG(variant >= 0 && variant <= BANDLU_GETRF_DIAG, 11,
                "band_getrf_ex: unknown variant");
     if (n > kMaxN || batch > INT_MAX) {
         set_error("band_getrf_ex: sizes too large");

@@ -81,8 +81,24 @@ __global__ __launch_bounds__(128) void getrf_split_kernel(WinParams P) {
     const int tid = threadIdx.x;
     const int L = tid & 63;
     const int64_t b = blockIdx.x;  // one matrix per workgroup
-    const int n = P.n, ku = P.ku, kv = kl + P.ku, ldab = int(P.ldab);
-    const Buf ab = make_buf(P.AB + b * P.strideAB, uint32_t(int64_t(ldab) * n * 8));
+    const int ku = P.ku, kv = kl + P.ku, ldab = int(P.ldab);
+    int n = P.n;
+    double *ABb = P.AB + b * P.strideAB;
+    int32_t *ipb = P.ipiv + b * P.strideP;
+    int j0 = 0;
+    if (P.resume) {
+        // after the diagonal-pivot kernel (getrf_diag.hpp): ipiv[n-1] > 0 says
+        // it factored the whole band, -(j0+1) that column j0 failed its check.
+        // Steps 0..j0-1 interchanged nothing, so the trailing band from column
+        // j0 on is a band problem of its own with the same kl and ku.
+        const int m = ipb[n - 1];
+        if (m > 0) return;
+        j0 = -m - 1;
+        n -= j0;
+        ABb += int64_t(j0) * ldab;
+        ipb += j0;
+    }
+    const Buf ab = make_buf(ABb, uint32_t(int64_t(ldab) * n * 8));
     __shared__ double s_l[2][32];    // multipliers of a step by row offset 1..kl
     __shared__ int s_pv[2][2];       // pivot offset and nonzero-pivot flag of a step
     __shared__ double s_col[2][64];  // a column for wave P, rows by offset from its first
@@ -195,7 +211,7 @@ __global__ __launch_bounds__(128) void getrf_split_kernel(WinParams P) {
     }
 
     // -------------------------------------------------------------- wave P --
-    const Buf pb = make_buf(P.ipiv + b * P.strideP, uint32_t(int64_t(n) * 4));
+    const Buf pb = make_buf(ipb, uint32_t(int64_t(n) * 4));
     // entering entries a(c+kl, c) of the 64 columns of this and the next block
     double E = buf_ld(ab, foff(L + kl, L));
     double En = buf_ld(ab, foff(64 + L + kl, 64 + L));
@@ -248,7 +264,7 @@ __global__ __launch_bounds__(128) void getrf_split_kernel(WinParams P) {
         const int lp = (u + p) & 63;
         const double piv = readlane_d(y, lp);
         const double rcp = readlane_d(rall, lp);  // 1/piv, formed beside the reduction
-        buf_st_i32(pb, L == 0 ? uint32_t(j) * 4u : kOutside, j + p + 1);
+        buf_st_i32(pb, L == 0 ? uint32_t(j) * 4u : kOutside, j0 + j + p + 1);
         const bool nzj = piv != 0.0;
         // the interchange (none for a zero pivot: then every candidate is zero
         // and p = 0)
@@ -277,7 +293,10 @@ __global__ __launch_bounds__(128) void getrf_split_kernel(WinParams P) {
             En = buf_ld(ab, foff(j + 65 + L + kl, j + 65 + L));
         }
     }
-    if (L == 0) P.info[b] = info;
+    if (L == 0) {
+        if (!P.resume) P.info[b] = info;
+        else if (info != 0 && P.info[b] == 0) P.info[b] = j0 + info;
+    }
 }
 
 // kernels of one CPL for H = LO..HI

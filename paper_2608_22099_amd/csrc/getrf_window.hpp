@@ -38,6 +38,8 @@ struct WinParams {
     int32_t *info;
     int64_t ldab, strideAB, strideP;
     int n, ku, batch;
+    int kl;      // read by the kernels that take kl at run time
+    int resume;  // two-wavefront kernel: continue where the diagonal-pivot kernel stopped
 };
 
 template <int G>

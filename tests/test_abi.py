@@ -72,8 +72,12 @@ def test_argument_validation(lib):
     assert lib.band_getrs(10, 2, 3, 1, fake, 8, fake, fake, 9, None) == -9
     # band_getrf_ex: argument 11 is the variant; a variant that cannot take the
     # sizes is refused before anything is enqueued
-    assert lib.band_getrf_ex(10, 2, 3, fake, 8, 80, fake, 10, fake, 1, 7, None) == -11
+    assert lib.band_getrf_ex(10, 2, 3, fake, 8, 80, fake, 10, fake, 1, 8, None) == -11
     assert lib.band_getrf_ex(10, 0, 3, fake, 4, 40, fake, 10, fake, 1, 6, None) == -1001
+    assert lib.band_getrf_ex(10, 0, 3, fake, 4, 40, fake, 10, fake, 1, 7, None) == -1001
+    assert lib.band_getrf_ex(100, 2, 30, fake, 35, 3500, fake, 100, fake, 1, 7, None) == -1001
+    assert lib.band_getrf_ex(100, 20, 22, fake, 63, 6300, fake, 100, fake, 1, 7, None) == -1001
+    assert lib.band_getrf_ex(100, 3, 3, fake, 70, 7000, fake, 100, fake, 1, 7, None) == -1001
     assert lib.band_getrf_ex(10, 2, 3, fake, 8, 80, fake, 10, fake, 1, -1, None) == -11
     assert lib.band_getrf_ex(100, 40, 3, fake, 84, 8400, fake, 100, fake, 1, 1, None) == -1001
     assert b"variant 1" in lib.band_last_error()
@@ -84,9 +88,16 @@ def test_argument_validation(lib):
 
 
 def test_variant_selection(lib):
-    W, G16, GEN, BLK, MF, SP = 1, 2, 3, 4, 5, 6
-    assert lib.band_getrf_variant(1000, 3, 3, 1) == SP
-    assert lib.band_getrf_variant(8192, 16, 16, 1) == SP
+    W, G16, GEN, BLK, MF, SP, DG = 1, 2, 3, 4, 5, 6, 7
+    assert lib.band_getrf_variant(1000, 3, 3, 1) == DG
+    assert lib.band_getrf_variant(8192, 16, 16, 1) == DG
+    assert lib.band_getrf_variant(300, 23, 17, 1) == DG
+    assert lib.band_getrf_variant(300, 20, 22, 1) == SP
+    assert lib.band_getrf_variant(300, 3, 24, 1) == DG
+    assert lib.band_getrf_variant(300, 15, 24, 1) == SP
+    assert lib.band_getrf_variant(300, 1, 24, 1) == DG
+    assert lib.band_getrf_variant(300, 2, 25, 1) == SP
+    assert lib.band_getrf_variant(256, 4, 4, 63) == DG
     assert lib.band_getrf_variant(16384, 2, 64, 1) == SP
     assert lib.band_getrf_variant(300, 15, 97, 1) == SP
     assert lib.band_getrf_variant(300, 0, 5, 1) == W

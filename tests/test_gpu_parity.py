@@ -230,6 +230,129 @@ def test_getrf_split_special():
         assert_bitwise(g[1], o[1], what)
 
 
+# The diagonal-pivot kernel must give the oracle's factors bit for bit
+# whether every column keeps its diagonal pivot (dominant bands), a column
+# fails the check (the two-wavefront kernel takes over there) or the first
+# one does (no diagonal shift: interchanges at most steps).
+DIAG_SHAPES = [(2, 1, 1), (3, 1, 1), (40, 1, 1), (300, 16, 16), (1000, 3, 3), (257, 1, 2),
+               (129, 5, 8), (200, 11, 20), (97, 18, 16), (70, 1, 24), (64, 2, 9), (66, 7, 13),
+               (500, 31, 1), (131, 9, 4), (77, 9, 17), (150, 6, 5), (90, 10, 15), (150, 23, 17),
+               (100, 14, 24)]
+
+
+def dominant_band(n, kl, ku, seed):
+    return random_band(n, kl, ku, seed, shift=4.0 * (kl + ku + 1))
+
+
+def check_exact(T, kl, ku, what, variant=None):
+    g, o = gpu_pipeline(T, kl, ku, variant=variant), oracle_pipeline(T, kl, ku)
+    assert np.array_equal(g[2], o[2]), f"{what}: ipiv"
+    assert g[3] == o[3], f"{what}: info {g[3]} vs {o[3]}"
+    assert_bitwise(g[1], o[1], what)
+    return g, o
+
+
+@pytest.mark.parametrize("n,kl,ku", DIAG_SHAPES)
+def test_getrf_diag_exact(n, kl, ku):
+    assert bandlu.band_getrf_variant(n, kl, ku) == "diag"
+    g, o = check_exact(dominant_band(n, kl, ku, 77 + n + ku), kl, ku, f"dominant n={n} kl={kl} ku={ku}")
+    assert np.array_equal(o[2], np.arange(1, n + 1))
+    check_exact(random_band(n, kl, ku, 78 + n + ku), kl, ku, f"random n={n} kl={kl} ku={ku}")
+
+
+@pytest.mark.parametrize("n,kl,ku,cols", [(300, 16, 16, (0, 1, 17, 35, 36, 37, 100, 298, 299)),
+                                          (129, 5, 8, (58, 59, 60, 61, 127, 128)),
+                                          (90, 10, 15, (16, 17, 33, 88))])
+def test_getrf_diag_resume(n, kl, ku, cols):
+    """A dominant band with one weak diagonal: the diagonal-pivot kernel stops
+    at that column (the last one has no candidates and never stops) and the
+    two-wavefront kernel factors the rest."""
+    for col in cols:
+        T = dominant_band(n, kl, ku, 900 + col)
+        T[col, col] = 1e-3  # T[j, i] is A[i, j]
+        g, o = check_exact(T, kl, ku, f"weak diagonal {col} n={n} kl={kl} ku={ku}")
+        assert (o[2][col] != col + 1) == (col < n - 1)
+        assert np.array_equal(o[2][:col], np.arange(1, col + 1))
+
+
+def test_getrf_diag_special():
+    """Zero columns (info, no interchange), NaN on and below the diagonal,
+    ties, pivots at and below DBL_MIN, a zero matrix and a zero column before
+    a failing one, all through the diagonal-pivot kernel."""
+    n, kl, ku = 120, 6, 5
+    cases = []
+    for k in (0, 7, 59, 119):
+        T = dominant_band(n, kl, ku, 5 + k)
+        T[k, :] = 0.0
+        cases.append((f"zero column {k}", T))
+    T = dominant_band(n, kl, ku, 99)
+    T[4, 4] = np.nan    # NaN pivot: kept, as partial pivoting keeps it
+    cases.append(("nan diagonal", T))
+    T = dominant_band(n, kl, ku, 98)
+    T[10, 12] = np.nan  # NaN candidate: never outranks the diagonal
+    cases.append(("nan below", T))
+    T = dominant_band(n, kl, ku, 97)
+    T[0, 1] = -T[0, 0]  # |candidate| = |diagonal|: the diagonal wins the tie
+    T[0, 3] = T[0, 0]
+    cases.append(("ties", T))
+    cases.append(("small", dominant_band(n, kl, ku, 96) * 1e-300))
+    cases.append(("subnormal", dominant_band(n, kl, ku, 95) * 1e-310))
+    cases.append(("zero matrix", np.zeros((n, n))))
+    T = dominant_band(n, kl, ku, 94)
+    T[20, :] = 0.0
+    T[50, 50] = 1e-6
+    cases.append(("zero column, then a failing one", T))
+    for what, T in cases:
+        g, o = check_exact(T, kl, ku, what, variant="diag")
+        if what.split()[-1].isdigit():
+            assert o[3] == int(what.split()[-1]) + 1
+    g, o = check_exact(cases[-1][1], kl, ku, "info across the hand-over", variant="diag")
+    assert o[3] == 21
+
+
+def test_getrf_diag_fill_rows_not_read():
+    """Fill slots hold garbage on entry; both kernels of the variant write
+    them (zeros, or fill-in after the hand-over)."""
+    n, kl, ku = 200, 8, 6
+    for weak in (None, 90):
+        T = dominant_band(n, kl, ku, 8)
+        if weak is not None:
+            T[weak, weak] = 1e-4
+        AB = bandlu.dense_to_band(to_dev(T), kl, ku)
+        AB[:, :kl] = float("nan")
+        ipiv, info = bandlu.band_getrf(AB, kl, ku, variant="diag")
+        o = oracle_pipeline(T, kl, ku)
+        got = AB.cpu().numpy()
+        kv = kl + ku
+        for j in range(n):  # slots outside the matrix keep what they held
+            for r in range(kl):
+                if r - kv + j < 0:
+                    got[j, r] = 0.0
+        assert np.array_equal(ipiv.cpu().numpy(), o[2]), weak
+        assert_bitwise(got, o[1], f"fill rows, weak diagonal {weak}")
+
+
+def test_getrf_diag_batched():
+    """Each matrix of a batch stops (or not) on its own."""
+    batch, n, kl, ku = 7, 180, 9, 11
+    Ts = []
+    for b in range(batch):
+        T = dominant_band(n, kl, ku, 700 + b) if b % 3 != 2 else random_band(n, kl, ku, 700 + b)
+        if b == 1:
+            T[77, 77] = 1e-5
+        if b == 4:
+            T[30, :] = 0.0
+        Ts.append(T)
+    T = np.stack(Ts)
+    AB = bandlu.dense_to_band_batched(to_dev(T), kl, ku)
+    ipiv, info = bandlu.band_getrf_batched(AB, kl, ku)
+    ABg, ipg, infg = AB.cpu().numpy(), ipiv.cpu().numpy(), info.cpu().numpy()
+    for b in range(batch):
+        o = oracle_pipeline(T[b], kl, ku)
+        assert np.array_equal(ipg[b], o[2]) and infg[b] == o[3], b
+        assert_bitwise(ABg[b], o[1], f"batch {b}")
+
+
 def test_getrf_singular_and_nan():
     n, kl, ku = 50, 3, 2
     for k in [0, 7, 49]:
