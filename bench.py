@@ -50,12 +50,14 @@ STEP_SOURCES = {
     "detect": ["detect.hip", "common.hpp"],
     "convert": ["convert.hip", "common.hpp"],
     "getrf": ["getrf.hip", "getrf_win64.hpp", "getrf_win2.hpp", "getrf_window.hpp", "getrf_g16.hpp",
-              "getrf_split.hpp", "getrf_blocked.hip", "getrf_mfma.hip", "wave.hpp", "bufio.hpp",
+              "getrf_split.hpp", "getrf_diag.hpp", "getrf_blocked.hip", "getrf_mfma.hip", "wave.hpp",
+              "bufio.hpp", "common.hpp"],
+    "getrs": ["getrs.hip", "getrs_ring.hpp", "getrs_ring.hip", "getrs_lane.hip", "bufio.hpp",
               "common.hpp"],
-    "getrs": ["getrs.hip", "getrs_ring.hpp", "getrs_ring.hip", "bufio.hpp", "common.hpp"],
 }
 # instantiation files of a step (one per parameter range), by name prefix
-STEP_PREFIXES = {"getrf": ("getrf_win_g", "getrf_split_c"), "getrs": ("getrs_ring_fwd", "getrs_ring_bwd")}
+STEP_PREFIXES = {"getrf": ("getrf_win_g", "getrf_split_c", "getrf_diag_ku"),
+                 "getrs": ("getrs_ring_fwd", "getrs_ring_bwd")}
 
 
 def source_hash(step):

@@ -205,6 +205,7 @@ int band_getrf_ex(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab, 
 #define BANDLU_GETRS_G16 2     /* register window, 16 lanes per system, many systems    */
 #define BANDLU_GETRS_RING 3    /* register ring plus factor columns staged in LDS       */
 #define BANDLU_GETRS_GENERIC 4 /* right-hand side in LDS or global memory, any band     */
+#define BANDLU_GETRS_LANE 5    /* one lane per row, kl+ku <= 63 and ldab <= 64          */
 int band_getrs_variant(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, int64_t batch);
 
 /*

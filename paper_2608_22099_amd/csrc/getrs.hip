@@ -19,6 +19,10 @@ int launch_getrs_ring(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const dou
                       int64_t ldab, int64_t strideAB, const int32_t *d_ipiv, int64_t strideP,
                       double *dB, int64_t ldb, int64_t strideB, int64_t batch, hipStream_t s);
 bool getrs_ring_fits(int64_t n, int64_t kl, int64_t ku, int64_t ldab);
+int launch_getrs_lane(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *dAB,
+                      int64_t ldab, int64_t strideAB, const int32_t *d_ipiv, int64_t strideP,
+                      double *dB, int64_t ldb, int64_t strideB, int64_t batch, hipStream_t s);
+bool getrs_lane_fits(int64_t n, int64_t kl, int64_t ku, int64_t ldab);
 
 namespace {
 
@@ -469,6 +473,7 @@ int select_getrs(int64_t n, int64_t kl, int64_t ku, int64_t ldab, int64_t nrhs, 
     const int64_t systems = batch * nrhs;
     if (systems >= 64 && g16_fits(n, kl, ku, nrhs, strideAB, strideP, ldb, strideB, batch))
         return BANDLU_GETRS_G16;
+    if (getrs_lane_fits(n, kl, ku, ldab)) return BANDLU_GETRS_LANE;
     if (getrs_ring_fits(n, kl, ku, ldab)) return BANDLU_GETRS_RING;
     if (window_fits(n, kl, ku, ldab)) return BANDLU_GETRS_WINDOW;
     return BANDLU_GETRS_GENERIC;
@@ -504,6 +509,7 @@ int launch_getrs(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *
         const bool ok = v == BANDLU_GETRS_G16 ? g16_fits(n, kl, ku, nrhs, strideAB, strideP, ldb, strideB, batch)
                       : v == BANDLU_GETRS_RING ? getrs_ring_fits(n, kl, ku, ldab)
                       : v == BANDLU_GETRS_WINDOW ? window_fits(n, kl, ku, ldab)
+                      : v == BANDLU_GETRS_LANE ? getrs_lane_fits(n, kl, ku, ldab)
                       : v == BANDLU_GETRS_GENERIC;
         if (!ok) {
             set_error("band_getrs: variant %d cannot solve n = %lld, kl = %lld, ku = %lld", v,
@@ -518,6 +524,9 @@ int launch_getrs(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *
         BANDLU_CHECK_LAUNCH("band_getrs (16 lanes per system)");
         return BANDLU_OK;
     }
+    if (v == BANDLU_GETRS_LANE)
+        return launch_getrs_lane(n, kl, ku, nrhs, dAB, ldab, strideAB, d_ipiv, strideP, dB, ldb,
+                                 strideB, batch, s);
     if (v == BANDLU_GETRS_RING)
         return launch_getrs_ring(n, kl, ku, nrhs, dAB, ldab, strideAB, d_ipiv, strideP, dB, ldb,
                                  strideB, batch, s);
@@ -615,7 +624,7 @@ extern "C" int band_getrs_ex(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, co
     BANDLU_ARG(ldb >= (n > 1 ? n : 1), 11, "band_getrs_ex: ldb < max(1, n)");
     BANDLU_ARG(batch <= 1 || strideB >= ldb * nrhs, 12, "band_getrs_ex: strideB < ldb*nrhs");
     BANDLU_ARG(batch >= 0, 13, "band_getrs_ex: batch < 0");
-    BANDLU_ARG(variant >= 0 && variant <= BANDLU_GETRS_GENERIC, 14, "band_getrs_ex: unknown variant");
+    BANDLU_ARG(variant >= 0 && variant <= BANDLU_GETRS_LANE, 14, "band_getrs_ex: unknown variant");
     if (n > kMaxN) {
         set_error("band_getrs_ex: n >= 2^31 is not supported");
         return BANDLU_ERR_UNSUPPORTED;

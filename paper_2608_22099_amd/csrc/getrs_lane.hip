@@ -1,0 +1,334 @@
+// Band solve for narrow bands (kl + ku <= 63, ldab <= 64) with the band
+// factors (xGBTRS, no transpose; the "lu(A) \ B" of Listings 1 and 2): one
+// wavefront per right-hand side, every row of the active window in a lane of
+// its own, so that a step is one fused multiply-add per lane and the chain
+// from one row to the next is a lane read, that fused multiply-add and (in
+// the backward pass) the division by the diagonal entry.
+//
+// Forward pass (L and the interchanges, rows j+1..j+kl): row r lives in lane
+// r mod 64.  Step j applies the interchange of ipiv[j] (the two lanes
+// exchange their values; the steps of a block of 64 that interchange are
+// marked in a scalar mask), takes b(j) from its lane and updates
+//   b(r) = fma(-l(r,j), b(j), b(r)),   r = j+1..j+min(kl, n-1-j).
+// The lane of row j keeps b(j), now final, for one coalesced store per block
+// and takes row j+64, loaded two blocks ahead.
+// Backward pass (U with its kl+ku superdiagonals): the same with j descending,
+//   x(j) = b(j) / u(j,j),  b(i) = fma(-u(i,j), x(j), b(i)),  i = j-kv..j-1,
+// where every lane forms x(j) from the scalar b(j) and a broadcast LDS read of
+// u(j,j).  The operations and their order per entry are those of the plain
+// column-oriented loops, so the solution is bitwise theirs.
+//
+// The factor columns reach LDS in chunks of 32 columns (a ring of 64 columns,
+// column c in slot c mod 64), one batch of 16-byte loads a chunk ahead; each
+// lane reads its entry of a column two steps before the step needs it.  Steps
+// issue no global memory operation.
+#include "bufio.hpp"
+#include "common.hpp"
+
+#include <utility>
+
+namespace bandlu {
+
+int launch_getrs_lane(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *dAB,
+                      int64_t ldab, int64_t strideAB, const int32_t *d_ipiv, int64_t strideP,
+                      double *dB, int64_t ldb, int64_t strideB, int64_t batch, hipStream_t s);
+bool getrs_lane_fits(int64_t n, int64_t kl, int64_t ku, int64_t ldab);
+
+namespace {
+
+constexpr int kChunk = 32;                        // factor columns per staged chunk
+constexpr int kStage = kChunk * 64 * 8 / 16 / 64;  // 16-byte loads per lane for a chunk (ldab <= 64)
+constexpr int kGuard = 64;                         // doubles of guard zone around the ring
+
+typedef unsigned lane_v4u __attribute__((ext_vector_type(4)));
+
+struct LaneParams {
+    const double *AB;
+    const int32_t *ipiv;
+    double *B;
+    int64_t ldab, strideAB, strideP, ldb, strideB;
+    int n, kl, kv, nrhs;
+};
+
+__device__ __forceinline__ unsigned long long lane_low(int k) {
+    return k >= 64 ? ~0ull : (1ull << k) - 1;
+}
+
+__device__ __forceinline__ unsigned long long lane_rotl(unsigned long long m, int k) {
+    return k == 0 ? m : (m << k) | (m >> (64 - k));
+}
+
+// a lane index and a stride hidden from loop-invariant motion, so that the
+// address of each step is formed in that step instead of 64 of them being
+// kept live across the loop
+__device__ __forceinline__ int lane_opaque_v(int v) {
+    asm volatile("" : "+v"(v));
+    return v;
+}
+__device__ __forceinline__ int lane_opaque_s(int v) {
+    asm volatile("" : "+s"(v));
+    return v;
+}
+
+// lane mask constants, formed where they are used from an opaque 1 (as
+// literals the optimiser keeps all of them live across the loop)
+__device__ __forceinline__ unsigned long long lane_one() {
+    unsigned long long o = 1;
+    asm volatile("" : "+s"(o));
+    return o;
+}
+__device__ __forceinline__ unsigned long long lane_bit(int q) { return lane_one() << q; }
+__device__ __forceinline__ unsigned long long lane_below(int q) {  // lanes 0..q-1, 0 <= q <= 63
+    const unsigned long long o = lane_one();
+    return (o << q) - o;
+}
+
+// the mask of a step, formed where it is used (an opaque copy keeps the
+// optimiser from hoisting all 64 rotations out of the loop)
+__device__ __forceinline__ unsigned long long lane_mask(unsigned long long m, int k) {
+    asm volatile("" : "+s"(m));
+    return lane_rotl(m, k);
+}
+
+// BULK (kl + ku <= 32): a lane changes rows in two batches per block of 64
+// steps (lanes 0-31, then 32-63), each with one coalesced store of the rows
+// it finishes; wider bands change the lane of each pivot row at its step.
+template <bool BULK>
+__global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
+    const int L = threadIdx.x;
+    const int64_t sys = blockIdx.x / P.nrhs;
+    const int64_t rhs = blockIdx.x - sys * P.nrhs;
+    const int n = P.n, kl = P.kl, kv = P.kv, ldab = int(P.ldab);
+    const Buf ab = make_buf(P.AB + sys * P.strideAB, uint32_t(int64_t(ldab) * n * 8));
+    const Buf bb = make_buf(P.B + sys * P.strideB + rhs * P.ldb, uint32_t(n) * 8u);
+    const Buf pb = make_buf(P.ipiv + sys * P.strideP, uint32_t(n) * 4u);
+    __shared__ double s_ring[kGuard + 64 * 64 + kGuard];
+    double *const ring = s_ring + kGuard;
+
+    // chunk k = factor columns 32k..32k+31, as in memory, into ring half k & 1
+    const int cbytes = kChunk * ldab * 8;
+    lane_v4u stg[kStage];
+    auto stage = [&](int k) __attribute__((always_inline)) {
+        const uint32_t base = uint32_t(k * kChunk * ldab) * 8u;
+#pragma unroll
+        for (int i = 0; i < kStage; ++i) {
+            const int o = (i * 64 + L) * 16;
+            stg[i] = __builtin_amdgcn_raw_buffer_load_b128(
+                ab.r, (k >= 0 && o < cbytes) ? base + uint32_t(o) : kOutside, 0, 0);
+        }
+    };
+    auto commit = [&](int k) __attribute__((always_inline)) {
+        char *dst = reinterpret_cast<char *>(ring + (k & 1) * kChunk * ldab);
+#pragma unroll
+        for (int i = 0; i < kStage; ++i) {
+            const int o = (i * 64 + L) * 16;
+            if (o < cbytes) *reinterpret_cast<lane_v4u *>(dst + o) = stg[i];
+        }
+    };
+    auto ldb_ = [&](int r) { return buf_ld(bb, (r >= 0 && r < n) ? uint32_t(r) * 8u : kOutside); };
+    auto stb_ = [&](int r, double v) { buf_st(bb, (r >= 0 && r < n) ? uint32_t(r) * 8u : kOutside, v); };
+    // ring index of (row, column) = (column slot q)*ldab + kv + row - column;
+    // for the row a lane holds that is q*(ldab-1) + kv + L, plus 64 in the
+    // lanes whose row is past the block of the column (minus 64 in the
+    // backward pass, for rows before it)
+    const int lp64 = L + 64, lm64 = L - 64;
+
+    // ------------------------------------------------------------ forward --
+    if (kl > 0 && n > 1) {
+        // at step j lane L holds row j + ((L - j) & 63)
+        double b = ldb_(L), bn1 = ldb_(64 + L), bn2 = ldb_(128 + L);
+        int myrow = L;
+        int ipv = buf_ld_i32(pb, L < n ? uint32_t(L) * 4u : kOutside);
+        int ipvn = buf_ld_i32(pb, 64 + L < n ? uint32_t(64 + L) * 4u : kOutside);
+        double yfin = 0.0;
+        stage(0);
+        commit(0);
+        stage(1);
+        const unsigned long long act0 = lane_low(kl) << 1;  // rows j+1..j+kl
+        auto lidx = [&](int q) __attribute__((always_inline)) {  // my multiplier in column slot q
+            const int lq = __builtin_amdgcn_inverse_ballot_w64(lane_below(q)) ? lp64 : L;
+            return q * (lane_opaque_s(ldab) - 1) + kv + lq;
+        };
+        double lr[2];  // this lane's multiplier for steps j and j+1
+        lr[0] = ring[lidx(0)];
+        lr[1] = ring[lidx(1)];
+        auto fstep = [&]<bool EDGE, int Q>(int j, unsigned long long swp) __attribute__((always_inline)) {
+            if (!(EDGE && j >= n - 1)) {
+                if ((swp >> Q) & 1ull) {
+                    // the interchange of ipiv[j]: rows j and ipiv[j]-1 exchange values
+                    const int lp = (__builtin_amdgcn_readlane(ipv, Q) - 1) & 63;
+                    const double vq = readlane_d(b, Q), vp = readlane_d(b, lp);
+                    b = __builtin_amdgcn_inverse_ballot_w64(lane_bit(Q)) ? vp
+                                                                     : (lane_opaque_v(L) == lp ? vq : b);
+                }
+                const double bj = readlane_d(b, Q);
+                const double l = lr[Q & 1];
+                lr[Q & 1] = ring[lidx((Q + 2) & 63)];
+                if constexpr (Q == 16 || Q == 48) {
+                    commit((j >> 5) + 1);
+                    stage((j >> 5) + 2);
+                }
+                unsigned long long act = lane_mask(act0, Q);
+                if (EDGE) act &= __builtin_amdgcn_ballot_w64(j + ((lane_opaque_v(L) - Q) & 63) < n);
+                if (__builtin_amdgcn_inverse_ballot_w64(act)) b = __builtin_fma(-l, bj, b);
+                if (!BULK && __builtin_amdgcn_inverse_ballot_w64(lane_bit(Q))) {  // the lane of row j
+                    yfin = bj;
+                    b = bn1;
+                }
+            }
+            if constexpr (BULK && (Q == 31 || Q == 63)) {
+                // lanes Q-31..Q have had their pivot steps: their rows are final
+                if (__builtin_amdgcn_inverse_ballot_w64(Q == 31 ? lane_below(32) : ~lane_below(32))) {
+                    stb_(myrow, b);
+                    myrow += 64;
+                    b = bn1;
+                }
+            }
+        };
+        for (int j0 = 0; j0 < (BULK ? n - 1 : n); j0 += 64) {
+            // steps of this block that interchange
+            const unsigned long long swp =
+                __builtin_amdgcn_ballot_w64(j0 + L < n - 1 && ipv != j0 + L + 1);
+            const bool edge = j0 + 64 >= n - 1;
+            [&]<int... Qs>(std::integer_sequence<int, Qs...>) __attribute__((always_inline)) {
+                if (edge)
+                    (fstep.template operator()<true, Qs>(j0 + Qs, swp), ...);
+                else
+                    (fstep.template operator()<false, Qs>(j0 + Qs, swp), ...);
+            }(std::make_integer_sequence<int, 64>{});
+            if (!BULK) {
+                // rows j0..j0+63 are final (row n-1, never a pivot, is in b)
+                const int r = j0 + L;
+                stb_(r, r == n - 1 ? b : yfin);
+            }
+            bn1 = bn2;
+            bn2 = ldb_(j0 + 192 + L);
+            ipv = ipvn;
+            ipvn = buf_ld_i32(pb, j0 + 128 + L < n ? uint32_t(j0 + 128 + L) * 4u : kOutside);
+        }
+        if (BULK) stb_(myrow, b);  // the rows no batch has stored
+        // the backward pass reads these stores back
+        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "agent");
+    }
+
+    // ----------------------------------------------------------- backward --
+    {
+        const int top = n - 1;
+        const int jt = top & ~63;
+        // at step j lane L holds row j - ((j - L) & 63)
+        int myrow = top - ((top - L) & 63);
+        double b = ldb_(myrow);
+        double bn1 = ldb_(jt - 64 + L), bn2 = ldb_(jt - 128 + L);
+        double xfin = 0.0;
+        const int kt = top >> 5;
+        stage(kt);
+        commit(kt);
+        if ((top & 31) < 16) {
+            stage(kt - 1);
+            commit(kt - 1);
+            stage(kt - 2);
+        } else {
+            stage(kt - 1);
+        }
+        // rows j-kv..j-1, relative to the lane of row j
+        const unsigned long long act0 = kv == 0 ? 0ull : lane_low(kv) << (64 - kv);
+        auto uidx = [&](int q) __attribute__((always_inline)) {  // my u(i, j) in column slot q
+            const int lq = (q < 63 && __builtin_amdgcn_inverse_ballot_w64(~lane_below(q + 1))) ? lm64 : L;
+            return q * (lane_opaque_s(ldab) - 1) + kv + lq;
+        };
+        double ur[2], dr[2];  // this lane's u(i,j) and u(j,j) for steps j and j-1
+        {
+            const int q0 = top & 63, q1 = (top - 1) & 63;
+            ur[q0 & 1] = ring[uidx(q0)];
+            dr[q0 & 1] = ring[q0 * ldab + kv];
+            ur[q1 & 1] = ring[uidx(q1)];
+            dr[q1 & 1] = ring[q1 * ldab + kv];
+        }
+        auto bstep = [&]<bool EDGE, int Q>(int j) __attribute__((always_inline)) {
+            if (!(EDGE && j > top)) {
+                const double bj = readlane_d(b, Q);
+                const double x = bj / dr[Q & 1];
+                const double u = ur[Q & 1];
+                {
+                    constexpr int Q2 = (Q - 2) & 63;
+                    ur[Q & 1] = ring[uidx(Q2)];
+                    dr[Q & 1] = ring[Q2 * lane_opaque_s(ldab) + kv];
+                }
+                if constexpr (Q == 16 || Q == 48) {
+                    commit((j >> 5) - 1);
+                    stage((j >> 5) - 2);
+                }
+                unsigned long long act = lane_mask(act0, Q);
+                if (EDGE) act &= __builtin_amdgcn_ballot_w64(j - ((Q - lane_opaque_v(L)) & 63) >= 0);
+                if (__builtin_amdgcn_inverse_ballot_w64(act)) b = __builtin_fma(-u, x, b);
+                if (__builtin_amdgcn_inverse_ballot_w64(lane_bit(Q))) {  // the lane of row j
+                    xfin = x;
+                    if (!BULK) b = bn1;
+                }
+            }
+            if constexpr (BULK && (Q == 32 || Q == 0)) {
+                // lanes Q..Q+31 have had their pivot steps, except in the first
+                // block those whose row is already below it
+                if (__builtin_amdgcn_inverse_ballot_w64(Q == 32 ? ~lane_below(32) : lane_below(32)) &&
+                    myrow >= j - Q) {
+                    if (myrow <= top) stb_(myrow, xfin);
+                    myrow -= 64;
+                    b = bn1;
+                }
+            }
+        };
+        for (int j0 = jt; j0 >= 0; j0 -= 64) {
+            const bool edge = j0 + 63 > top || j0 == 0;
+            [&]<int... Qs>(std::integer_sequence<int, Qs...>) __attribute__((always_inline)) {
+                if (edge)
+                    (bstep.template operator()<true, 63 - Qs>(j0 + 63 - Qs), ...);
+                else
+                    (bstep.template operator()<false, 63 - Qs>(j0 + 63 - Qs), ...);
+            }(std::make_integer_sequence<int, 64>{});
+            if (!BULK) {
+                const int r = j0 + L;
+                if (r <= top) stb_(r, xfin);
+            }
+            bn1 = bn2;
+            bn2 = ldb_(j0 - 192 + L);
+        }
+    }
+}
+
+}  // namespace
+
+bool getrs_lane_fits(int64_t n, int64_t kl, int64_t ku, int64_t ldab) {
+    return kl + ku <= 63 && ldab <= 64 && ldab * n * 8 <= kMaxBufferBytes && n * 8 <= kMaxBufferBytes;
+}
+
+int launch_getrs_lane(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *dAB,
+                      int64_t ldab, int64_t strideAB, const int32_t *d_ipiv, int64_t strideP,
+                      double *dB, int64_t ldb, int64_t strideB, int64_t batch, hipStream_t s) {
+    if (n == 0 || nrhs == 0 || batch == 0) return BANDLU_OK;
+    if (!getrs_lane_fits(n, kl, ku, ldab)) {
+        set_error("band_getrs: the lane solve needs kl+ku <= 63 and ldab <= 64");
+        return BANDLU_ERR_UNSUPPORTED;
+    }
+    LaneParams P;
+    P.AB = dAB;
+    P.ipiv = d_ipiv;
+    P.B = dB;
+    P.ldab = ldab;
+    P.strideAB = strideAB;
+    P.strideP = strideP;
+    P.ldb = ldb;
+    P.strideB = strideB;
+    P.n = (int)n;
+    P.kl = (int)kl;
+    P.kv = (int)(kl + ku);
+    P.nrhs = (int)nrhs;
+    if (kl + ku <= 32)
+        hipLaunchKernelGGL(getrs_lane_kernel<true>, dim3((unsigned)(batch * nrhs)), dim3(64), 0, s, P);
+    else
+        hipLaunchKernelGGL(getrs_lane_kernel<false>, dim3((unsigned)(batch * nrhs)), dim3(64), 0, s, P);
+    BANDLU_CHECK_LAUNCH("band_getrs (lane per row)");
+    return BANDLU_OK;
+}
+
+}  // namespace bandlu

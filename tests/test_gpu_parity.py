@@ -510,6 +510,52 @@ def test_getrs_window_exact(n, kl, ku):
         assert_bitwise(Bg.cpu().numpy(), xo, f"{variant} getrs n={n} kl={kl} ku={ku}")
 
 
+LANE_SHAPES = [(1, 0, 0), (2, 1, 0), (2, 0, 1), (3, 1, 1), (63, 5, 3), (64, 16, 16), (65, 16, 16),
+               (66, 2, 7), (127, 20, 23), (128, 10, 43), (129, 1, 61), (200, 0, 20), (300, 16, 16),
+               (1000, 3, 3), (8191, 16, 16), (641, 21, 21), (97, 0, 63)]
+
+
+@pytest.mark.parametrize("n,kl,ku", LANE_SHAPES)
+def test_getrs_lane_exact(n, kl, ku):
+    """The lane-per-row solve, bitwise against the oracle, with interchanges
+    (factors of a random band) and without (a dominant band), and with
+    several right-hand sides."""
+    for shift, nrhs in ((0.0, 1), (4.0 * (kl + ku + 1), 3)):
+        T = random_band(n, kl, ku, 61 + n + kl + ku, shift=shift)
+        ABo = oracle_pipeline(T, kl, ku)[1]
+        ipo = oracle_pipeline(T, kl, ku)[2]
+        B = np.random.default_rng(n + kl).standard_normal((nrhs, n))
+        xo = B.copy()
+        oracle.gbtrs(ABo, kl, ku, ipo, xo)
+        Bg = to_dev(B)
+        if nrhs == 1:
+            assert bandlu.band_getrs_variant(n, kl, ku) == "lane"
+        bandlu.band_getrs(to_dev(ABo), kl, ku, to_dev(ipo), Bg, variant="lane")
+        assert_bitwise(Bg.cpu().numpy(), xo, f"lane getrs n={n} kl={kl} ku={ku} nrhs={nrhs}")
+
+
+def test_getrs_lane_batched_and_special():
+    """Batched systems through the lane solve; a right-hand side with a NaN,
+    infinities and zeros."""
+    batch, n, kl, ku = 5, 150, 6, 9
+    T = np.stack([random_band(n, kl, ku, 800 + b, shift=(0.0 if b % 2 else 30.0)) for b in range(batch)])
+    outs = [oracle_pipeline(T[b], kl, ku) for b in range(batch)]
+    AB = np.stack([o[1] for o in outs])
+    ip = np.stack([o[2] for o in outs]).astype(np.int32)
+    B = np.random.default_rng(5).standard_normal((batch, 2, n))
+    B[1, 0, 7] = np.nan
+    B[2, 1, 100] = np.inf
+    B[3, 0, :] = 0.0
+    xo = B.copy()
+    for b in range(batch):
+        oracle.gbtrs(AB[b], kl, ku, ip[b], xo[b])
+    Bg = to_dev(B)
+    bandlu.band_getrs_batched(to_dev(AB), kl, ku, to_dev(ip), Bg, variant="lane")
+    got = Bg.cpu().numpy()
+    for b in range(batch):
+        assert_bitwise(got[b], xo[b], f"batch {b}")
+
+
 def test_getrs_ring_batched_and_padded():
     batch, n, kl, ku, nrhs = 5, 400, 70, 90, 2
     T = np.stack([random_band(n, kl, ku, 1400 + b) for b in range(batch)])
