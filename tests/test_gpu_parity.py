@@ -262,7 +262,8 @@ def test_getrf_diag_exact(n, kl, ku):
 
 @pytest.mark.parametrize("n,kl,ku,cols", [(300, 16, 16, (0, 1, 17, 35, 36, 37, 100, 298, 299)),
                                           (129, 5, 8, (58, 59, 60, 61, 127, 128)),
-                                          (90, 10, 15, (16, 17, 33, 88))])
+                                          (90, 10, 15, (16, 17, 33, 88)),
+                                          (2000, 16, 16, (71, 72, 73, 107, 500, 1000, 1511, 1998))])
 def test_getrf_diag_resume(n, kl, ku, cols):
     """A dominant band with one weak diagonal: the diagonal-pivot kernel stops
     at that column (the last one has no candidates and never stops) and the
@@ -308,6 +309,15 @@ def test_getrf_diag_special():
             assert o[3] == int(what.split()[-1]) + 1
     g, o = check_exact(cases[-1][1], kl, ku, "info across the hand-over", variant="diag")
     assert o[3] == 21
+    # long bands: a zero column and tiny pivots inside a chunk away from both
+    # ends (the chunk is undone and replayed step by step)
+    for col in (500, 719):
+        T = dominant_band(2000, 16, 16, 70 + col)
+        T[col, :] = 0.0
+        g, o = check_exact(T, 16, 16, f"zero column {col}, n=2000", variant="diag")
+        assert o[3] == col + 1
+    T = dominant_band(2000, 16, 16, 71) * 1e-310
+    check_exact(T, 16, 16, "subnormal pivots, n=2000", variant="diag")
 
 
 def test_getrf_diag_fill_rows_not_read():
