@@ -36,11 +36,7 @@ bool getrs_lane_fits(int64_t n, int64_t kl, int64_t ku, int64_t ldab);
 
 namespace {
 
-constexpr int kChunk = 32;                        // factor columns per staged chunk
-constexpr int kStage = kChunk * 64 * 8 / 16 / 64;  // 16-byte loads per lane for a chunk (ldab <= 64)
-constexpr int kGuard = 64;                         // doubles of guard zone around the ring
-
-typedef unsigned lane_v4u __attribute__((ext_vector_type(4)));
+constexpr int kChunk = 32;  // factor columns per staged chunk
 
 struct LaneParams {
     const double *AB;
@@ -58,15 +54,11 @@ __device__ __forceinline__ unsigned long long lane_rotl(unsigned long long m, in
     return k == 0 ? m : (m << k) | (m >> (64 - k));
 }
 
-// a lane index and a stride hidden from loop-invariant motion, so that the
-// address of each step is formed in that step instead of 64 of them being
-// kept live across the loop
+// a lane index hidden from loop-invariant motion, so that what a step forms
+// from it is formed in that step instead of 64 values being kept live across
+// the loop
 __device__ __forceinline__ int lane_opaque_v(int v) {
     asm volatile("" : "+v"(v));
-    return v;
-}
-__device__ __forceinline__ int lane_opaque_s(int v) {
-    asm volatile("" : "+s"(v));
     return v;
 }
 
@@ -102,36 +94,31 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
     const Buf ab = make_buf(P.AB + sys * P.strideAB, uint32_t(int64_t(ldab) * n * 8));
     const Buf bb = make_buf(P.B + sys * P.strideB + rhs * P.ldb, uint32_t(n) * 8u);
     const Buf pb = make_buf(P.ipiv + sys * P.strideP, uint32_t(n) * 4u);
-    __shared__ double s_ring[kGuard + 64 * 64 + kGuard];
-    double *const ring = s_ring + kGuard;
+    // ring of 64 factor columns: column c in slot c mod 64, its entry of row r
+    // at position r mod 64 (ldab <= 64 keeps them apart), so that the lane of
+    // row r reads slot q at q*64 + L: an address with no per-step arithmetic
+    __shared__ double ring[64 * 64];
 
-    // chunk k = factor columns 32k..32k+31, as in memory, into ring half k & 1
-    const int cbytes = kChunk * ldab * 8;
-    lane_v4u stg[kStage];
+    // chunk k = factor columns 32k..32k+31: lane t loads band row t of each
+    double stg[kChunk];
     auto stage = [&](int k) __attribute__((always_inline)) {
-        const uint32_t base = uint32_t(k * kChunk * ldab) * 8u;
 #pragma unroll
-        for (int i = 0; i < kStage; ++i) {
-            const int o = (i * 64 + L) * 16;
-            stg[i] = __builtin_amdgcn_raw_buffer_load_b128(
-                ab.r, (k >= 0 && o < cbytes) ? base + uint32_t(o) : kOutside, 0, 0);
+        for (int q = 0; q < kChunk; ++q) {
+            const int c = k * kChunk + q;
+            stg[q] = buf_ld(ab, (k >= 0 && L < ldab && c < n) ? uint32_t(c * ldab + L) * 8u : kOutside);
         }
     };
+    // ... and stores it at the position of its row, c - kv + t (lanes past
+    // ldab write zeros at positions no band row of the column has)
     auto commit = [&](int k) __attribute__((always_inline)) {
-        char *dst = reinterpret_cast<char *>(ring + (k & 1) * kChunk * ldab);
 #pragma unroll
-        for (int i = 0; i < kStage; ++i) {
-            const int o = (i * 64 + L) * 16;
-            if (o < cbytes) *reinterpret_cast<lane_v4u *>(dst + o) = stg[i];
+        for (int q = 0; q < kChunk; ++q) {
+            const int c = k * kChunk + q;
+            ring[(c & 63) * 64 + ((c - kv + L) & 63)] = stg[q];
         }
     };
     auto ldb_ = [&](int r) { return buf_ld(bb, (r >= 0 && r < n) ? uint32_t(r) * 8u : kOutside); };
     auto stb_ = [&](int r, double v) { buf_st(bb, (r >= 0 && r < n) ? uint32_t(r) * 8u : kOutside, v); };
-    // ring index of (row, column) = (column slot q)*ldab + kv + row - column;
-    // for the row a lane holds that is q*(ldab-1) + kv + L, plus 64 in the
-    // lanes whose row is past the block of the column (minus 64 in the
-    // backward pass, for rows before it)
-    const int lp64 = L + 64, lm64 = L - 64;
 
     // ------------------------------------------------------------ forward --
     if (kl > 0 && n > 1) {
@@ -145,16 +132,15 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
         commit(0);
         stage(1);
         const unsigned long long act0 = lane_low(kl) << 1;  // rows j+1..j+kl
-        auto lidx = [&](int q) __attribute__((always_inline)) {  // my multiplier in column slot q
-            const int lq = __builtin_amdgcn_inverse_ballot_w64(lane_below(q)) ? lp64 : L;
-            return q * (lane_opaque_s(ldab) - 1) + kv + lq;
-        };
         double lr[2];  // this lane's multiplier for steps j and j+1
-        lr[0] = ring[lidx(0)];
-        lr[1] = ring[lidx(1)];
-        auto fstep = [&]<bool EDGE, int Q>(int j, unsigned long long swp) __attribute__((always_inline)) {
+        lr[0] = ring[L];
+        lr[1] = ring[64 + L];
+        // SWP: the block has interchanges (a copy without the test runs the
+        // blocks that have none)
+        auto fstep = [&]<bool EDGE, bool SWP, int Q>(int j, unsigned long long swp)
+                         __attribute__((always_inline)) {
             if (!(EDGE && j >= n - 1)) {
-                if ((swp >> Q) & 1ull) {
+                if (SWP && ((swp >> Q) & 1ull)) {
                     // the interchange of ipiv[j]: rows j and ipiv[j]-1 exchange values
                     const int lp = (__builtin_amdgcn_readlane(ipv, Q) - 1) & 63;
                     const double vq = readlane_d(b, Q), vp = readlane_d(b, lp);
@@ -163,7 +149,7 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
                 }
                 const double bj = readlane_d(b, Q);
                 const double l = lr[Q & 1];
-                lr[Q & 1] = ring[lidx((Q + 2) & 63)];
+                lr[Q & 1] = ring[((Q + 2) & 63) * 64 + L];
                 if constexpr (Q == 16 || Q == 48) {
                     commit((j >> 5) + 1);
                     stage((j >> 5) + 2);
@@ -192,9 +178,11 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
             const bool edge = j0 + 64 >= n - 1;
             [&]<int... Qs>(std::integer_sequence<int, Qs...>) __attribute__((always_inline)) {
                 if (edge)
-                    (fstep.template operator()<true, Qs>(j0 + Qs, swp), ...);
+                    (fstep.template operator()<true, true, Qs>(j0 + Qs, swp), ...);
+                else if (swp != 0)
+                    (fstep.template operator()<false, true, Qs>(j0 + Qs, swp), ...);
                 else
-                    (fstep.template operator()<false, Qs>(j0 + Qs, swp), ...);
+                    (fstep.template operator()<false, false, Qs>(j0 + Qs, swp), ...);
             }(std::make_integer_sequence<int, 64>{});
             if (!BULK) {
                 // rows j0..j0+63 are final (row n-1, never a pivot, is in b)
@@ -233,17 +221,13 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
         }
         // rows j-kv..j-1, relative to the lane of row j
         const unsigned long long act0 = kv == 0 ? 0ull : lane_low(kv) << (64 - kv);
-        auto uidx = [&](int q) __attribute__((always_inline)) {  // my u(i, j) in column slot q
-            const int lq = (q < 63 && __builtin_amdgcn_inverse_ballot_w64(~lane_below(q + 1))) ? lm64 : L;
-            return q * (lane_opaque_s(ldab) - 1) + kv + lq;
-        };
         double ur[2], dr[2];  // this lane's u(i,j) and u(j,j) for steps j and j-1
         {
             const int q0 = top & 63, q1 = (top - 1) & 63;
-            ur[q0 & 1] = ring[uidx(q0)];
-            dr[q0 & 1] = ring[q0 * ldab + kv];
-            ur[q1 & 1] = ring[uidx(q1)];
-            dr[q1 & 1] = ring[q1 * ldab + kv];
+            ur[q0 & 1] = ring[q0 * 64 + L];
+            dr[q0 & 1] = ring[q0 * 65];
+            ur[q1 & 1] = ring[q1 * 64 + L];
+            dr[q1 & 1] = ring[q1 * 65];
         }
         auto bstep = [&]<bool EDGE, int Q>(int j) __attribute__((always_inline)) {
             if (!(EDGE && j > top)) {
@@ -252,8 +236,8 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
                 const double u = ur[Q & 1];
                 {
                     constexpr int Q2 = (Q - 2) & 63;
-                    ur[Q & 1] = ring[uidx(Q2)];
-                    dr[Q & 1] = ring[Q2 * lane_opaque_s(ldab) + kv];
+                    ur[Q & 1] = ring[Q2 * 64 + L];
+                    dr[Q & 1] = ring[Q2 * 65];  // u(j-2, j-2): row j-2 sits at position Q2
                 }
                 if constexpr (Q == 16 || Q == 48) {
                     commit((j >> 5) - 1);
