@@ -25,17 +25,22 @@
 // ahead into staging registers and copied into an LDS buffer (double
 // buffered) when the chunk begins, so no step waits on global memory.  A
 // step j
-//   - takes row j (u(j,j..j+ku)) and 1/u(j,j) from the lane of row j with
-//     lane reads into scalar registers;
-//   - checks the kl candidates and exits on the first failure;
+//   - takes u(j,j) and 1/u(j,j) from the lane of row j with lane reads into
+//     scalar registers, and checks the kl candidates, exiting on the first
+//     failure;
+//   - takes the rest of row j, u(j,j+1..j+ku), as vector registers: every
+//     lane writes its row to LDS at the end of a step and the next pivot row
+//     is read back at once as a broadcast, so the read is in flight during
+//     the step boundary (two lane reads per entry cost more);
 //   - reads column j+ku+1 from the chunk buffer into the slot column j-1 has
 //     left, each lane its own row;
 //   - forms the multipliers and the rank-1 update in the lanes of rows
-//     j+1..j+kl, ku fused multiply-adds per lane;
+//     j+1..j+kl, ku fused multiply-adds per lane, column j+1 first: row
+//     j+1 is then final and its lane forms 1/u(j+1,j+1), one stage of the
+//     division between every one or two of the other updates;
 //   - stores column j of the factors (U entries kept in their rows' lanes
 //     since those rows were pivot rows, the multipliers, and zeros in the
-//     fill slots): one coalesced store;
-//   - forms 1/u(j+1,j+1) in the lane of row j+1.
+//     fill slots): one coalesced store.
 // The lane masks of a step live in scalar registers, so its control never
 // waits for a vector result, except for the one test of the candidates.
 // One chunk of steps is unrolled, so that every register index is a
@@ -53,8 +58,10 @@
 
 namespace bandlu {
 
-// steps per chunk for upper bandwidth KU: a multiple of the slot period, >= 32
-constexpr int diag_chunk(int KU) { return (KU + 2) * ((32 + KU + 1) / (KU + 2)); }
+// steps per chunk for upper bandwidth KU: a multiple of the slot period, at
+// least 16 and no longer than that needs (every step of a chunk is unrolled,
+// and longer chunks no longer fit the instruction cache)
+constexpr int diag_chunk(int KU) { return (KU + 2) * ((16 + KU + 1) / (KU + 2)); }
 // Largest kl for KU: the live rows (from j-KU, whose U entries are still to
 // be stored, to j+KU+1+kl, the last row column j+KU+1 reaches) need a lane
 // each, and the 2kl+KU+1 rows a column store covers must fall in distinct
@@ -67,12 +74,48 @@ constexpr int kDiagMaxKu = 24;
 
 typedef unsigned diag_v4u __attribute__((ext_vector_type(4)));
 
+// 1/v by the hardware's correctly rounded division sequence (scale, reciprocal
+// estimate, two Newton refinements, quotient correction, fix-up of special
+// operands), one instruction per stage, so that a caller can place other work
+// between the dependent stages; bitwise the quotient 1.0 / v.
+struct DiagRecip {
+    double den, d, nn, r, e, q;
+    bool flag;
+    template <int G>
+    __device__ __forceinline__ void stage() {
+        if constexpr (G == 0) {
+            bool f0;
+            d = __builtin_amdgcn_div_scale(1.0, den, false, &f0);
+            nn = __builtin_amdgcn_div_scale(1.0, den, true, &flag);
+        } else if constexpr (G == 1) {
+            r = __builtin_amdgcn_rcp(d);
+        } else if constexpr (G == 2) {
+            e = __builtin_fma(-d, r, 1.0);
+        } else if constexpr (G == 3) {
+            r = __builtin_fma(r, e, r);
+        } else if constexpr (G == 4) {
+            e = __builtin_fma(-d, r, 1.0);
+        } else if constexpr (G == 5) {
+            r = __builtin_fma(r, e, r);
+        } else if constexpr (G == 6) {
+            q = nn * r;
+        } else if constexpr (G == 7) {
+            e = __builtin_fma(-d, q, nn);
+        } else if constexpr (G == 8) {
+            q = __builtin_amdgcn_div_fmas(e, r, q, flag);
+        } else {
+            q = __builtin_amdgcn_div_fixup(q, den, 1.0);
+        }
+    }
+    static constexpr int kStages = 10;
+};
+
 template <int KU>
 __global__ __launch_bounds__(64) void getrf_diag_kernel(WinParams P) {
-    constexpr int S = KU + 2;           // window slots: columns j-1..j+KU
-    constexpr int C = diag_chunk(KU);   // steps (and band columns) per chunk
+    constexpr int S = KU + 2;               // window slots: columns j-1..j+KU
+    constexpr int C = diag_chunk(KU);       // steps (and band columns) per chunk
     constexpr int NST = (C * 64) / 128 + 1;  // 16-byte loads per lane for a chunk (ldab <= 64)
-    constexpr int G = 64;               // guard doubles on both sides of a chunk buffer
+    constexpr int G = 64;                   // guard doubles on both sides of a chunk buffer
     const int L = threadIdx.x;
     const int64_t b = blockIdx.x;
     const int n = P.n, kl = P.kl, kv = kl + KU, ldab = int(P.ldab);
@@ -81,6 +124,9 @@ __global__ __launch_bounds__(64) void getrf_diag_kernel(WinParams P) {
     // original band columns of a chunk, laid out as in memory (ldab apart),
     // with guard zones: every lane reads its slot without a bounds test
     __shared__ double s_col[2][G + C * 64 + G];
+    // every lane's row after a step (entry k of the row at [k][lane]), read
+    // back whole by the next step for its pivot row
+    __shared__ double s_u[KU + 1][64];
 
     for (int j = L; j < n - 1; j += 64) ipiv[j] = j + 1;
 
@@ -109,6 +155,7 @@ __global__ __launch_bounds__(64) void getrf_diag_kernel(WinParams P) {
     // at step s lane L holds row s + eof(s), eof(s) in [-KU, 63-KU]
     auto eof = [&](int s) { return ((L - s + KU) & 63) - KU; };
     double x[S];
+    double un[KU + 1];  // the next step's pivot row, u(j+1, j+1..j+1+KU)
     {
         const int r = eof(0);
 #pragma unroll
@@ -118,6 +165,10 @@ __global__ __launch_bounds__(64) void getrf_diag_kernel(WinParams P) {
             x[c] = buf_ld(ab, ok ? uint32_t(c * ldab + kv + d) * 8u : kOutside);
         }
         x[S - 1] = 0.0;
+#pragma unroll
+        for (int k = 1; k <= KU; ++k) s_u[k][L] = x[k];
+#pragma unroll
+        for (int k = 1; k <= KU; ++k) un[k] = s_u[k][0];
         stage(0);
         commit(0);
         stage(1);
@@ -148,17 +199,17 @@ __global__ __launch_bounds__(64) void getrf_diag_kernel(WinParams P) {
             act &= __builtin_amdgcn_ballot_w64(s + e < n);
             st &= __builtin_amdgcn_ballot_w64(rs >= 0 && rs < n);
         }
-        double u[KU + 1];
-#pragma unroll
-        for (int k = 0; k <= KU; ++k) u[k] = readlane_d(x[(X + k) % S], ls);
-        const double piv = u[0];
+        const double piv = readlane_d(x[X], ls);
         // a candidate with a larger key than the diagonal's: an ordered
         // comparison of magnitudes is that test, NaNs included (a NaN
         // candidate ranks last, a NaN diagonal first)
-        if (__builtin_amdgcn_ballot_w64(__builtin_amdgcn_inverse_ballot_w64(act) && fabs(x[X]) > fabs(piv))) {
+        if (__builtin_amdgcn_ballot_w64(fabs(x[X]) > fabs(piv)) & act) {
             stop = s;
             return false;
         }
+        double u[KU + 1];
+#pragma unroll
+        for (int k = 1; k <= KU; ++k) u[k] = un[k];
         // column s+KU+1 enters the window, in the slot column s-1 has left
         // (lanes of other rows read a harmless entry: no row uses its slot
         // for that column)
@@ -166,7 +217,7 @@ __global__ __launch_bounds__(64) void getrf_diag_kernel(WinParams P) {
         const double rcp = readlane_d(rn, ls);
         double l = x[X] * rcp;
         const unsigned hi = unsigned(__double_as_longlong(piv) >> 32);
-        if (((hi >> 20) & 0x7ffu) - 1u >= 0x7feu) {
+        if (__builtin_expect(((hi >> 20) & 0x7ffu) - 1u >= 0x7feu, 0)) {
             // zero, below DBL_MIN, infinite or NaN: the pivoting loop's choices
             if (piv == 0.0) {
                 act = 0;  // nothing to eliminate
@@ -175,12 +226,37 @@ __global__ __launch_bounds__(64) void getrf_diag_kernel(WinParams P) {
                 l = x[X] / piv;
             }
         }
+        // Row s+1 is final once column s+1 is updated: its lane forms the
+        // next reciprocal at once, each stage of the division followed by a
+        // share of the other columns' updates, which do not depend on it.
+        // With nothing to eliminate (a zero pivot) it is formed on its own.
         if (__builtin_amdgcn_inverse_ballot_w64(act)) {
             x[X] = l;
+            x[(X + 1) % S] = __builtin_fma(-l, u[1], x[(X + 1) % S]);
+            DiagRecip dv;
+            dv.den = x[(X + 1) % S];
+            [&]<int... Gs>(std::integer_sequence<int, Gs...>) __attribute__((always_inline)) {
+                (
+                    [&] {
+                        dv.template stage<Gs>();
+                        constexpr int NF = KU - 1, NG = DiagRecip::kStages;
 #pragma unroll
-            for (int k = 1; k <= KU; ++k) x[(X + k) % S] = __builtin_fma(-l, u[k], x[(X + k) % S]);
+                        for (int f = Gs * NF / NG; f < (Gs + 1) * NF / NG; ++f)
+                            x[(X + 2 + f) % S] = __builtin_fma(-l, u[2 + f], x[(X + 2 + f) % S]);
+                        __builtin_amdgcn_sched_barrier(0);
+                    }(),
+                    ...);
+            }(std::make_integer_sequence<int, DiagRecip::kStages>{});
+            rn = dv.q;
             asm volatile("" ::: "memory");  // keep the block a branch under an exec mask
         }
+        if (__builtin_expect(act == 0, 0)) rn = 1.0 / x[(X + 1) % S];
+        // this lane's row as it now stands; the lane of row s+1 holds the
+        // next pivot row, read back at once (a broadcast) for the next step
+#pragma unroll
+        for (int k = 1; k <= KU; ++k) s_u[k][L] = x[(X + 1 + k) % S];
+#pragma unroll
+        for (int k = 1; k <= KU; ++k) un[k] = s_u[k][(s + 1) & 63];
         // column s of the factors: U rows s-KU..s, multipliers s+1..s+kl, and
         // zeros in the fill slots of rows s-kv..s-KU-1 (those lanes belong to
         // rows 64 further on, which column s does not reach)
@@ -190,8 +266,6 @@ __global__ __launch_bounds__(64) void getrf_diag_kernel(WinParams P) {
             const uint32_t voff = __builtin_amdgcn_inverse_ballot_w64(st) ? uint32_t(kv + rel) * 8u : kOutside;
             buf_st_so(ab, voff, uint32_t(s * ldab) * 8u, up ? x[X] : 0.0);
         }
-        // row s+1 is final: its lane forms the next reciprocal
-        rn = 1.0 / x[(X + 1) % S];
         m_act = rotr(m_act, 63);
         m_up = rotr(m_up, 63);
         m_st = rotr(m_st, 63);
@@ -238,6 +312,7 @@ __global__ __launch_bounds__(64) void getrf_diag_kernel(WinParams P) {
     }
     if (L == 0) P.info[b] = info;
 }
+
 
 template <int LO, int HI>
 struct DiagRange {
