@@ -101,11 +101,16 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
 
     // chunk k = factor columns 32k..32k+31: lane t loads band row t of each
     double stg[kChunk];
+    // (lanes past ldab and columns outside the matrix read out of range: the
+    // offset, below 2^32 for every column a chunk names, gets the top bit by
+    // arithmetic; a test there becomes a divergent branch around every load)
+    const uint32_t lane_out = L < ldab ? 0u : kOutside;
     auto stage = [&](int k) __attribute__((always_inline)) {
 #pragma unroll
         for (int q = 0; q < kChunk; ++q) {
             const int c = k * kChunk + q;
-            stg[q] = buf_ld(ab, (k >= 0 && L < ldab && c < n) ? uint32_t(c * ldab + L) * 8u : kOutside);
+            const uint32_t out = lane_out | ((k >= 0) & (c < n) ? 0u : kOutside);
+            stg[q] = buf_ld(ab, (uint32_t(c * ldab + L) * 8u) | out);
         }
     };
     // ... and stores it at the position of its row, c - kv + t (lanes past
@@ -132,9 +137,13 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
         commit(0);
         stage(1);
         const unsigned long long act0 = lane_low(kl) << 1;  // rows j+1..j+kl
-        double lr[2];  // this lane's multiplier for steps j and j+1
-        lr[0] = ring[L];
-        lr[1] = ring[64 + L];
+        double lr[4];  // this lane's multipliers for steps j..j+3
+#pragma unroll
+        for (int q = 0; q < 4; ++q) lr[q] = ring[q * 64 + L];
+        // the last step's update as formed, before the select keeps it in
+        // the lanes that take part: the lane of row j always does, so b(j)
+        // can be read there, one instruction earlier on the chain
+        double t = b;
         // SWP: the block has interchanges (a copy without the test runs the
         // blocks that have none)
         auto fstep = [&]<bool EDGE, bool SWP, int Q>(int j, unsigned long long swp)
@@ -147,16 +156,23 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
                     b = __builtin_amdgcn_inverse_ballot_w64(lane_bit(Q)) ? vp
                                                                      : (lane_opaque_v(L) == lp ? vq : b);
                 }
-                const double bj = readlane_d(b, Q);
-                const double l = lr[Q & 1];
-                lr[Q & 1] = ring[((Q + 2) & 63) * 64 + L];
+                const double bj = readlane_d((EDGE || SWP) ? b : t, Q);
+                const double l = lr[Q & 3];
+                lr[Q & 3] = ring[((Q + 4) & 63) * 64 + L];
                 if constexpr (Q == 16 || Q == 48) {
                     commit((j >> 5) + 1);
                     stage((j >> 5) + 2);
                 }
-                unsigned long long act = lane_mask(act0, Q);
-                if (EDGE) act &= __builtin_amdgcn_ballot_w64(j + ((lane_opaque_v(L) - Q) & 63) < n);
-                if (__builtin_amdgcn_inverse_ballot_w64(act)) b = __builtin_fma(-l, bj, b);
+                t = __builtin_fma(-l, bj, b);
+                if (EDGE) {
+                    unsigned long long act = lane_mask(act0, Q);
+                    act &= __builtin_amdgcn_ballot_w64(j + ((lane_opaque_v(L) - Q) & 63) < n);
+                    if (__builtin_amdgcn_inverse_ballot_w64(act)) b = t;
+                } else if (((lane_opaque_v(L) - Q - 1) & 63) < kl) {
+                    // rows j+1..j+kl, by a vector compare: a select on a lane
+                    // mask made by scalar instructions waits longer for it
+                    b = t;
+                }
                 if (!BULK && __builtin_amdgcn_inverse_ballot_w64(lane_bit(Q))) {  // the lane of row j
                     yfin = bj;
                     b = bn1;
@@ -229,9 +245,10 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
             ur[q1 & 1] = ring[q1 * 64 + L];
             dr[q1 & 1] = ring[q1 * 65];
         }
+        double t = b;  // as in the forward pass: the last step's update as formed
         auto bstep = [&]<bool EDGE, int Q>(int j) __attribute__((always_inline)) {
             if (!(EDGE && j > top)) {
-                const double bj = readlane_d(b, Q);
+                const double bj = readlane_d(EDGE ? b : t, Q);
                 const double x = bj / dr[Q & 1];
                 const double u = ur[Q & 1];
                 {
@@ -243,9 +260,14 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
                     commit((j >> 5) - 1);
                     stage((j >> 5) - 2);
                 }
-                unsigned long long act = lane_mask(act0, Q);
-                if (EDGE) act &= __builtin_amdgcn_ballot_w64(j - ((Q - lane_opaque_v(L)) & 63) >= 0);
-                if (__builtin_amdgcn_inverse_ballot_w64(act)) b = __builtin_fma(-u, x, b);
+                t = __builtin_fma(-u, x, b);
+                if (EDGE) {
+                    unsigned long long act = lane_mask(act0, Q);
+                    act &= __builtin_amdgcn_ballot_w64(j - ((Q - lane_opaque_v(L)) & 63) >= 0);
+                    if (__builtin_amdgcn_inverse_ballot_w64(act)) b = t;
+                } else if (((Q - lane_opaque_v(L) - 1) & 63) < kv) {
+                    b = t;  // rows j-kv..j-1
+                }
                 if (__builtin_amdgcn_inverse_ballot_w64(lane_bit(Q))) {  // the lane of row j
                     xfin = x;
                     if (!BULK) b = bn1;
@@ -263,7 +285,9 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
             }
         };
         for (int j0 = jt; j0 >= 0; j0 -= 64) {
-            const bool edge = j0 + 63 > top || j0 == 0;
+            // (with no superdiagonals no lane takes part in a step, and b(j)
+            // is read from b)
+            const bool edge = j0 + 63 > top || j0 == 0 || kv == 0;
             [&]<int... Qs>(std::integer_sequence<int, Qs...>) __attribute__((always_inline)) {
                 if (edge)
                     (bstep.template operator()<true, 63 - Qs>(j0 + 63 - Qs), ...);
