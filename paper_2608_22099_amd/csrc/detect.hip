@@ -201,11 +201,29 @@ __global__ __launch_bounds__(kThreads) void detect_flat_kernel(FlatParams P) {
     const int lane = tid & 63;
     const int n = int(P.n);
     int kl_t = 0, ku_t = 0;
+    // the loads of a workgroup's next chunk are issued before it scans the
+    // current one, so that its reads stay in flight across chunks
+    auto load = [&](int64_t k, dbl2 *v) __attribute__((always_inline)) {
+        const int64_t f0 = k * kFlatChunk;
+        const dbl2 *base = reinterpret_cast<const dbl2 *>(P.A + f0);
+#pragma unroll
+        for (int u = 0; u < kFlatU; ++u) {
+            const int e = u * (kThreads * 2) + tid * 2;
+            v[u] = f0 + e < P.total ? __builtin_nontemporal_load(base + (e >> 1)) : dbl2{0.0, 0.0};
+        }
+    };
+    dbl2 v[kFlatU], vn[kFlatU];
+    if (int64_t(blockIdx.x) < P.nchunks) load(blockIdx.x, v);
     for (int64_t k = blockIdx.x; k < P.nchunks; k += gridDim.x) {
         const int64_t mat = BATCHED ? k / P.chunks_per_matrix : 0;
         unsigned long long *out = P.out + 3 * mat;
+        if (k + gridDim.x < P.nchunks) load(k + gridDim.x, vn);
         if (CAPS && __hip_atomic_load(out + 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0ull) {
-            if (BATCHED) continue;
+            if (BATCHED) {
+#pragma unroll
+                for (int u = 0; u < kFlatU; ++u) v[u] = vn[u];
+                continue;
+            }
             break;
         }
         const int64_t f0 = k * kFlatChunk;
@@ -213,13 +231,6 @@ __global__ __launch_bounds__(kThreads) void detect_flat_kernel(FlatParams P) {
         const int64_t col0 = BATCHED ? (fm >> P.log2n) : fm / P.n;
         const int i0 = int(fm - col0 * P.n);
         const int c0 = int(col0);
-        const dbl2 *base = reinterpret_cast<const dbl2 *>(P.A + f0);
-        dbl2 v[kFlatU];
-#pragma unroll
-        for (int u = 0; u < kFlatU; ++u) {
-            const int e = u * (kThreads * 2) + tid * 2;
-            v[u] = f0 + e < P.total ? __builtin_nontemporal_load(base + (e >> 1)) : dbl2{0.0, 0.0};
-        }
 #pragma unroll
         for (int u = 0; u < kFlatU; ++u) {
             const int e = u * (kThreads * 2) + tid * 2;
@@ -237,6 +248,8 @@ __global__ __launch_bounds__(kThreads) void detect_flat_kernel(FlatParams P) {
             if (v[u].x != 0.0) { kl_t = max(kl_t, d); ku_t = max(ku_t, -d); }
             if (v[u].y != 0.0) { kl_t = max(kl_t, d + 1); ku_t = max(ku_t, -d - 1); }
         }
+#pragma unroll
+        for (int u = 0; u < kFlatU; ++u) v[u] = vn[u];
         if (BATCHED) {
             const int a = wave_max_i32(kl_t), b = wave_max_i32(ku_t);
             if (lane == 0) {
