@@ -260,8 +260,8 @@ def test_getrf_diag_exact(n, kl, ku):
     check_exact(random_band(n, kl, ku, 78 + n + ku), kl, ku, f"random n={n} kl={kl} ku={ku}")
 
 
-@pytest.mark.parametrize("n,kl,ku,cols", [(300, 16, 16, (0, 1, 17, 35, 36, 37, 100, 298, 299)),
-                                          (129, 5, 8, (58, 59, 60, 61, 127, 128)),
+@pytest.mark.parametrize("n,kl,ku,cols", [(300, 16, 16, (0, 1, 2, 3, 17, 18, 19, 35, 36, 37, 53, 54, 100, 298, 299)),
+                                          (129, 5, 8, (19, 20, 39, 40, 58, 59, 60, 61, 127, 128)),
                                           (90, 10, 15, (16, 17, 33, 88)),
                                           (2000, 16, 16, (71, 72, 73, 107, 500, 1000, 1511, 1998))])
 def test_getrf_diag_resume(n, kl, ku, cols):
@@ -318,6 +318,22 @@ def test_getrf_diag_special():
         assert o[3] == col + 1
     T = dominant_band(2000, 16, 16, 71) * 1e-310
     check_exact(T, 16, 16, "subnormal pivots, n=2000", variant="diag")
+
+
+def _column_scales(n):
+    """Powers of ten from 1e-300 to 1e300 (and a subnormal scale) by column."""
+    e = np.array([-300, -150, -20, 0, 20, 150, 300, -306, -310])
+    return 10.0 ** np.tile(e, n // e.size + 1)[:n]
+
+
+def test_getrf_diag_extreme_magnitudes():
+    """Columns scaled from 1e-310 to 1e300 (pivot choices unchanged, pivots
+    and their reciprocals across the exponent range, subnormal pivots that
+    divide instead), through the diagonal-pivot kernel, bitwise."""
+    for n, kl, ku in ((400, 16, 16), (300, 3, 3), (250, 7, 24)):
+        T = dominant_band(n, kl, ku, 4242 + ku) * _column_scales(n)[:, None]  # row j of T is column j of A
+        assert bandlu.band_getrf_variant(n, kl, ku) == "diag"
+        check_exact(T, kl, ku, f"scaled columns n={n} kl={kl} ku={ku}")
 
 
 def test_getrf_diag_fill_rows_not_read():
@@ -564,6 +580,24 @@ def test_getrs_lane_batched_and_special():
     got = Bg.cpu().numpy()
     for b in range(batch):
         assert_bitwise(got[b], xo[b], f"batch {b}")
+
+
+def test_getrs_lane_extreme_magnitudes():
+    """The lane solve with a diagonal of U from 1e-310 to 1e300 and
+    right-hand sides with tiny, huge and subnormal entries (the division's
+    scaled cases), bitwise against the oracle."""
+    for n, kl, ku in ((700, 16, 16), (500, 21, 21), (300, 2, 5)):
+        T = dominant_band(n, kl, ku, 4343 + ku) * _column_scales(n)[:, None]
+        o = oracle_pipeline(T, kl, ku)
+        rng = np.random.default_rng(n + ku)
+        B = rng.standard_normal((2, n)) * 10.0 ** rng.choice([-300, -200, 0, 200, 300], size=(2, n))
+        B[0, ::13] = 5e-324
+        xo = B.copy()
+        oracle.gbtrs(o[1], kl, ku, o[2], xo)
+        Bg = to_dev(B)
+        assert bandlu.band_getrs_variant(n, kl, ku) == "lane"
+        bandlu.band_getrs(to_dev(o[1]), kl, ku, to_dev(o[2]), Bg)
+        assert_bitwise(Bg.cpu().numpy(), xo, f"scaled lane getrs n={n} kl={kl} ku={ku}")
 
 
 def test_getrs_ring_batched_and_padded():
