@@ -109,7 +109,7 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
 #pragma unroll
         for (int q = 0; q < kChunk; ++q) {
             const int c = k * kChunk + q;
-            const uint32_t out = lane_out | ((k >= 0) & (c < n) ? 0u : kOutside);
+            const uint32_t out = lane_out | (((k >= 0) & (c < n)) ? 0u : kOutside);
             stg[q] = buf_ld(ab, (uint32_t(c * ldab + L) * 8u) | out);
         }
     };
@@ -133,9 +133,10 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
         int ipv = buf_ld_i32(pb, L < n ? uint32_t(L) * 4u : kOutside);
         int ipvn = buf_ld_i32(pb, 64 + L < n ? uint32_t(64 + L) * 4u : kOutside);
         double yfin = 0.0;
+        double bnx;  // b rows and interchanges two blocks ahead, loaded early in a block
+        int ipx;
         stage(0);
         commit(0);
-        stage(1);
         const unsigned long long act0 = lane_low(kl) << 1;  // rows j+1..j+kl
         double lr[4];  // this lane's multipliers for steps j..j+3
 #pragma unroll
@@ -159,10 +160,13 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
                 const double bj = readlane_d((EDGE || SWP) ? b : t, Q);
                 const double l = lr[Q & 3];
                 lr[Q & 3] = ring[((Q + 4) & 63) * 64 + L];
-                if constexpr (Q == 16 || Q == 48) {
-                    commit((j >> 5) + 1);
-                    stage((j >> 5) + 2);
-                }
+                // chunk k+1 is loaded at the first step of chunk k and enters
+                // the ring 27 steps later, before step 32k+28 reads its first
+                // column: no staged register lives across the end of a block,
+                // where the copies of the block join (a join would wait there
+                // for every load in flight)
+                if constexpr (Q == 0 || Q == 32) stage((j >> 5) + 1);
+                if constexpr (Q == 27 || Q == 59) commit((j >> 5) + 1);
                 t = __builtin_fma(-l, bj, b);
                 if (EDGE) {
                     unsigned long long act = lane_mask(act0, Q);
@@ -177,6 +181,11 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
                     yfin = bj;
                     b = bn1;
                 }
+            }
+            if constexpr (Q == 1) {
+                const int j0 = j - 1;
+                bnx = ldb_(j0 + 192 + L);
+                ipx = buf_ld_i32(pb, j0 + 128 + L < n ? uint32_t(j0 + 128 + L) * 4u : kOutside);
             }
             if constexpr (BULK && (Q == 31 || Q == 63)) {
                 // lanes Q-31..Q have had their pivot steps: their rows are final
@@ -206,9 +215,9 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
                 stb_(r, r == n - 1 ? b : yfin);
             }
             bn1 = bn2;
-            bn2 = ldb_(j0 + 192 + L);
+            bn2 = bnx;
             ipv = ipvn;
-            ipvn = buf_ld_i32(pb, j0 + 128 + L < n ? uint32_t(j0 + 128 + L) * 4u : kOutside);
+            ipvn = ipx;
         }
         if (BULK) stb_(myrow, b);  // the rows no batch has stored
         // the backward pass reads these stores back
@@ -225,14 +234,18 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
         double b = ldb_(myrow);
         double bn1 = ldb_(jt - 64 + L), bn2 = ldb_(jt - 128 + L);
         double xfin = 0.0;
+        double bnx;  // b rows two blocks ahead, loaded early in a block
+        // chunk k-1 is loaded at the first step of chunk k (j = 32k+31) and
+        // enters the ring at j = 32k+4, after step 32k+2 has read the last
+        // column of chunk k it needs; the chunks whose points come before
+        // the top row are handled here
         const int kt = top >> 5;
         stage(kt);
         commit(kt);
-        if ((top & 31) < 16) {
+        if ((top & 31) < 4) {
             stage(kt - 1);
             commit(kt - 1);
-            stage(kt - 2);
-        } else {
+        } else if ((top & 31) < 31) {
             stage(kt - 1);
         }
         // rows j-kv..j-1, relative to the lane of row j
@@ -256,10 +269,8 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
                     ur[Q & 1] = ring[Q2 * 64 + L];
                     dr[Q & 1] = ring[Q2 * 65];  // u(j-2, j-2): row j-2 sits at position Q2
                 }
-                if constexpr (Q == 16 || Q == 48) {
-                    commit((j >> 5) - 1);
-                    stage((j >> 5) - 2);
-                }
+                if constexpr (Q == 31 || Q == 63) stage((j >> 5) - 1);
+                if constexpr (Q == 4 || Q == 36) commit((j >> 5) - 1);
                 t = __builtin_fma(-u, x, b);
                 if (EDGE) {
                     unsigned long long act = lane_mask(act0, Q);
@@ -273,6 +284,7 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
                     if (!BULK) b = bn1;
                 }
             }
+            if constexpr (Q == 62) bnx = ldb_(j - 62 - 192 + L);
             if constexpr (BULK && (Q == 32 || Q == 0)) {
                 // lanes Q..Q+31 have had their pivot steps, except in the first
                 // block those whose row is already below it
@@ -299,7 +311,7 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
                 if (r <= top) stb_(r, xfin);
             }
             bn1 = bn2;
-            bn2 = ldb_(j0 - 192 + L);
+            bn2 = bnx;
         }
     }
 }
