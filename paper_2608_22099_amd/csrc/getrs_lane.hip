@@ -122,6 +122,23 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
             ring[(c & 63) * 64 + ((c - kv + L) & 63)] = stg[q];
         }
     };
+    // columns q0, q0+1 of chunk k, for the backward steps, which spread a
+    // chunk's loads and ring stores over 16 steps each
+    auto stage2 = [&]<int q0>(int k) __attribute__((always_inline)) {
+#pragma unroll
+        for (int q = q0; q < q0 + 2; ++q) {
+            const int c = k * kChunk + q;
+            const uint32_t out = lane_out | (((k >= 0) & (c < n)) ? 0u : kOutside);
+            stg[q] = buf_ld(ab, (uint32_t(c * ldab + L) * 8u) | out);
+        }
+    };
+    auto commit2 = [&]<int q0>(int k) __attribute__((always_inline)) {
+#pragma unroll
+        for (int q = q0; q < q0 + 2; ++q) {
+            const int c = k * kChunk + q;
+            ring[(c & 63) * 64 + ((c - kv + L) & 63)] = stg[q];
+        }
+    };
     auto ldb_ = [&](int r) { return buf_ld(bb, (r >= 0 && r < n) ? uint32_t(r) * 8u : kOutside); };
     auto stb_ = [&](int r, double v) { buf_st(bb, (r >= 0 && r < n) ? uint32_t(r) * 8u : kOutside, v); };
 
@@ -164,7 +181,9 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
                 // the ring 27 steps later, before step 32k+28 reads its first
                 // column: no staged register lives across the end of a block,
                 // where the copies of the block join (a join would wait there
-                // for every load in flight)
+                // for every load in flight). Spread over the steps as in the
+                // backward pass, the loads and stores measured slower here:
+                // this chain has fewer idle issue slots to hide them in.
                 if constexpr (Q == 0 || Q == 32) stage((j >> 5) + 1);
                 if constexpr (Q == 27 || Q == 59) commit((j >> 5) + 1);
                 t = __builtin_fma(-l, bj, b);
@@ -235,19 +254,18 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
         double bn1 = ldb_(jt - 64 + L), bn2 = ldb_(jt - 128 + L);
         double xfin = 0.0;
         double bnx;  // b rows two blocks ahead, loaded early in a block
-        // chunk k-1 is loaded at the first step of chunk k (j = 32k+31) and
-        // enters the ring at j = 32k+4, after step 32k+2 has read the last
-        // column of chunk k it needs; the chunks whose points come before
-        // the top row are handled here
+        // chunk k-1 is loaded over the top 16 steps of chunk k (columns 2p,
+        // 2p+1 at j = 32k+31-p; a burst of 32 loads, or of 32 ring stores,
+        // holds up the step chain behind it) and each pair enters the ring
+        // 12 steps later, by j = 32k+4, before step 32k+1 reads the chunk's
+        // last column. No staged register lives across the end of a block. Chunk kt-1 is also loaded and stored here whole: the
+        // steps above the top row that would load part of it do not run
+        // (the pairs the loop loads again are the same values).
         const int kt = top >> 5;
         stage(kt);
         commit(kt);
-        if ((top & 31) < 4) {
-            stage(kt - 1);
-            commit(kt - 1);
-        } else if ((top & 31) < 31) {
-            stage(kt - 1);
-        }
+        stage(kt - 1);
+        commit(kt - 1);
         // rows j-kv..j-1, relative to the lane of row j
         const unsigned long long act0 = kv == 0 ? 0ull : lane_low(kv) << (64 - kv);
         double ur[2], dr[2];  // this lane's u(i,j) and u(j,j) for steps j and j-1
@@ -269,8 +287,9 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
                     ur[Q & 1] = ring[Q2 * 64 + L];
                     dr[Q & 1] = ring[Q2 * 65];  // u(j-2, j-2): row j-2 sits at position Q2
                 }
-                if constexpr (Q == 31 || Q == 63) stage((j >> 5) - 1);
-                if constexpr (Q == 4 || Q == 36) commit((j >> 5) - 1);
+                constexpr int Qh = Q & 31;
+                if constexpr (Qh >= 16) stage2.template operator()<2 * (31 - Qh)>((j >> 5) - 1);
+                if constexpr (Qh >= 4 && Qh < 20) commit2.template operator()<2 * (19 - Qh)>((j >> 5) - 1);
                 t = __builtin_fma(-u, x, b);
                 if (EDGE) {
                     unsigned long long act = lane_mask(act0, Q);
