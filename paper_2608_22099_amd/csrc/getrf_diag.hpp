@@ -269,6 +269,16 @@ __global__ __launch_bounds__(64) void getrf_diag_kernel(WinParams P) {
         m_act = rotr(m_act, 63);
         m_up = rotr(m_up, 63);
         m_st = rotr(m_st, 63);
+        if constexpr (Q == C - 1) {
+            // the next chunk into LDS (its loads were issued a chunk ago),
+            // and the loads of the one after it. Here, not after the chunk:
+            // only a chunk that ran all its steps gets here, so the wait for
+            // the loads counts this chunk's column stores as issued after
+            // them (where the early exits join, it waits for those too).
+            const int k = (s - (C - 1)) / C;
+            commit(k + 1);
+            stage(k + 2);
+        }
         return true;
     };
     auto chunk = [&]<bool EDGE>(int s0) __attribute__((always_inline)) -> bool {
@@ -282,10 +292,6 @@ __global__ __launch_bounds__(64) void getrf_diag_kernel(WinParams P) {
         const bool interior = s0 >= kv && s0 + C + KU + kl + 1 <= n;
         const bool go = interior ? chunk.template operator()<false>(s0) : chunk.template operator()<true>(s0);
         if (!go || s0 + C >= n) break;
-        // the next chunk into LDS (its loads were issued a chunk ago), and the
-        // loads of the one after it
-        commit(k + 1);
-        stage(k + 2);
     }
     if (stop >= 0) {
         // the band as it stands before step `stop`: entries that earlier steps
