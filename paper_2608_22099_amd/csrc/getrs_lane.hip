@@ -155,7 +155,7 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
         stage(0);
         commit(0);
         const unsigned long long act0 = lane_low(kl) << 1;  // rows j+1..j+kl
-        double lr[4];  // this lane's multipliers for steps j..j+3
+        double lr[8];  // this lane's multipliers, by step mod 8, read 4-5 steps ahead
 #pragma unroll
         for (int q = 0; q < 4; ++q) lr[q] = ring[q * 64 + L];
         // the last step's update as formed, before the select keeps it in
@@ -175,8 +175,12 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
                                                                      : (lane_opaque_v(L) == lp ? vq : b);
                 }
                 const double bj = readlane_d((EDGE || SWP) ? b : t, Q);
-                const double l = lr[Q & 3];
-                lr[Q & 3] = ring[((Q + 4) & 63) * 64 + L];
+                const double l = lr[Q & 7];
+                if constexpr ((Q & 1) == 0) {
+                    // two steps' multipliers, one slot apart: one LDS read
+                    lr[(Q + 4) & 7] = ring[((Q + 4) & 63) * 64 + L];
+                    lr[(Q + 5) & 7] = ring[((Q + 5) & 63) * 64 + L];
+                }
                 // chunk k+1 is loaded at the first step of chunk k and enters
                 // the ring 27 steps later, before step 32k+28 reads its first
                 // column: no staged register lives across the end of a block,
@@ -268,24 +272,38 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
         commit(kt - 1);
         // rows j-kv..j-1, relative to the lane of row j
         const unsigned long long act0 = kv == 0 ? 0ull : lane_low(kv) << (64 - kv);
-        double ur[2], dr[2];  // this lane's u(i,j) and u(j,j) for steps j and j-1
+        // this lane's u(i,j) and u(j,j) by step mod 4, read 2-3 steps ahead
+        // (two steps at a time, at odd steps); steps top..top-2 read here,
+        // placed by value selects (a slot index known only at run time would
+        // put the arrays in scratch memory)
+        double ur[4] = {}, dr[4] = {};
         {
-            const int q0 = top & 63, q1 = (top - 1) & 63;
-            ur[q0 & 1] = ring[q0 * 64 + L];
-            dr[q0 & 1] = ring[q0 * 65];
-            ur[q1 & 1] = ring[q1 * 64 + L];
-            dr[q1 & 1] = ring[q1 * 65];
+#pragma unroll
+            for (int d = 0; d < 3; ++d) {
+                const int q = (top - d) & 63;
+                const double uv = ring[q * 64 + L], dv = ring[q * 65];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    ur[i] = (q & 3) == i ? uv : ur[i];
+                    dr[i] = (q & 3) == i ? dv : dr[i];
+                }
+            }
         }
         double t = b;  // as in the forward pass: the last step's update as formed
         auto bstep = [&]<bool EDGE, int Q>(int j) __attribute__((always_inline)) {
             if (!(EDGE && j > top)) {
                 const double bj = readlane_d(EDGE ? b : t, Q);
-                const double x = bj / dr[Q & 1];
-                const double u = ur[Q & 1];
-                {
-                    constexpr int Q2 = (Q - 2) & 63;
-                    ur[Q & 1] = ring[Q2 * 64 + L];
-                    dr[Q & 1] = ring[Q2 * 65];  // u(j-2, j-2): row j-2 sits at position Q2
+                const double x = bj / dr[Q & 3];
+                const double u = ur[Q & 3];
+                if constexpr (Q & 1) {
+                    // steps j-2 and j-3, one slot apart: one LDS read each for
+                    // the lane's entries and for the diagonal (row j-2 sits at
+                    // position Q2)
+                    constexpr int Q2 = (Q - 2) & 63, Q3 = (Q - 3) & 63;
+                    ur[Q2 & 3] = ring[Q2 * 64 + L];
+                    ur[Q3 & 3] = ring[Q3 * 64 + L];
+                    dr[Q2 & 3] = ring[Q2 * 65];
+                    dr[Q3 & 3] = ring[Q3 * 65];
                 }
                 constexpr int Qh = Q & 31;
                 if constexpr (Qh >= 16) stage2.template operator()<2 * (31 - Qh)>((j >> 5) - 1);
