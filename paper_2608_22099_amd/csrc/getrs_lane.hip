@@ -262,9 +262,10 @@ __global__ __launch_bounds__(64) void getrs_lane_kernel(LaneParams P) {
         // 2p+1 at j = 32k+31-p; a burst of 32 loads, or of 32 ring stores,
         // holds up the step chain behind it) and each pair enters the ring
         // 12 steps later, by j = 32k+4, before step 32k+1 reads the chunk's
-        // last column. No staged register lives across the end of a block. Chunk kt-1 is also loaded and stored here whole: the
-        // steps above the top row that would load part of it do not run
-        // (the pairs the loop loads again are the same values).
+        // last column. No staged register lives across the end of a block.
+        // Chunk kt-1 is also loaded and stored here whole: the steps above
+        // the top row that would load part of it do not run (the pairs the
+        // loop loads again are the same values).
         const int kt = top >> 5;
         stage(kt);
         commit(kt);
