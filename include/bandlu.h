@@ -76,7 +76,8 @@ int band_detect(const double *dA, int64_t n, int64_t lda, int64_t kl_cap, int64_
                 int64_t *d_out, void *stream);
 
 /*
- * band_detect_batched -- band_detect over `batch` matrices of the same n;
+ * band_detect_batched -- step 1 (Sec. II-A cost I(N), Sec. III-A) over
+ * many independent systems: band_detect over `batch` matrices of the same n;
  * matrix b starts at dA + b*strideA (strideA >= lda*n).  Writes
  * d_out[3b..3b+2] per matrix as band_detect does, and d_max[0..2] =
  * {max kl, max ku, any exceeded} over the batch (the bandwidths a single
@@ -101,7 +102,9 @@ int dense_to_band(const double *dA, int64_t n, int64_t lda, int64_t kl, int64_t 
                   double *dAB, int64_t ldab, void *stream);
 
 /*
- * dense_to_band_batched -- dense_to_band for `batch` matrices: matrix b at
+ * dense_to_band_batched -- step 2 (Sec. II-A cost C(N); Listing 2's
+ * conversion) over many independent systems: dense_to_band for `batch`
+ * matrices: matrix b at
  * dA + b*strideA, its band at dAB + b*strideAB (strideAB >= ldab*n).
  */
 int dense_to_band_batched(const double *dA, int64_t n, int64_t lda, int64_t strideA,
@@ -136,7 +139,9 @@ int band_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab, int
                int32_t *d_info, void *stream);
 
 /*
- * band_getrf_batched -- band_getrf on `batch` independent matrices of the same
+ * band_getrf_batched -- step 3 (Sec. II-A cost f(N); Sec. III-A banded LU,
+ * xGBTRF) over many independent systems: band_getrf on `batch` independent
+ * matrices of the same
  * n, kl, ku: band b at dAB + b*strideAB (strideAB >= ldab*n), pivots at
  * d_ipiv + b*strideP (strideP >= n), info at d_info[b].
  */
@@ -159,7 +164,8 @@ int band_getrs(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *dA
                const int32_t *d_ipiv, double *dB, int64_t ldb, void *stream);
 
 /*
- * band_getrs_batched -- band_getrs on `batch` systems: factors at
+ * band_getrs_batched -- the solve of Listings 1 and 2 ("lu(A) \ B", xGBTRS)
+ * over many independent systems: band_getrs on `batch` systems: factors at
  * dAB + b*strideAB, pivots at d_ipiv + b*strideP, right-hand sides at
  * dB + b*strideB (strideB >= ldb*nrhs).
  */
@@ -224,7 +230,9 @@ int band_getrs_ex(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double 
                   double *dB, int64_t ldb, int64_t strideB, int64_t batch, int variant,
                   void *stream);
 
-/* Text for a status code (static storage). */
+/* Text for a status code (static storage).  The codes follow the LAPACK
+ * convention that the paper's callees (xGBTRF, xGETRF; Sec. III-A) use for
+ * invalid arguments, plus the two library codes above. */
 const char *band_status_string(int status);
 
 /* Details of the last failure on the calling thread ("" if none). */

@@ -13,8 +13,8 @@ shape (n, ldab); batched arrays add a leading batch dimension.
 
 Names follow the paper's path (Sec. II-A, Listing 2): band_detect (identify),
 dense_to_band (convert), band_getrf / band_getrf_batched (specialised LU),
-band_getrs / band_getrs_batched (solve), and the host policy
-speedup_predicate / structure_aware_lu (Sec. II-B speedup constraint).
+band_getrs / band_getrs_batched (solve).  The host policy of Listing 2 (the
+Sec. II-B speedup constraint and structure_aware_lu) is in ``policy``.
 """
 from __future__ import annotations
 
@@ -266,49 +266,3 @@ def band_getrs_batched(AB, kl, ku, ipiv, B, variant=None):
         _call("band_getrs_ex", n, kl, ku, nrhs, _ptr(AB), ldab, sAB, _ptr(ipiv), sP, _ptr(B), ldb,
               sB, batch, _getrs_code(variant), _stream())
     return B
-
-
-# ------------------------------------------------------------- host policy --
-def op_counts(n, kl, ku):
-    """Operation counts of Sec. II-A for one n x n matrix with bandwidths (kl, ku):
-    identify I = n^2 reads, convert C = (2kl+ku+1) n band slots, specialised
-    f = 2 n kl (kl+ku+1) flops (banded LU including pivot fill), generic
-    F = 2 n^3 / 3 flops (dense LU)."""
-    I = n * n
-    C = (2 * kl + ku + 1) * n
-    f = 2 * n * kl * (kl + ku + 1)
-    F = 2.0 * n ** 3 / 3.0
-    return I, C, f, F
-
-
-def speedup_predicate(n, kl, ku):
-    """Sec. II-B speedup constraint I + C + f < F: take the banded branch."""
-    I, C, f, F = op_counts(n, kl, ku)
-    return I + C + f < F
-
-
-class BandLU:
-    """Result of structure_aware_lu on the banded branch."""
-
-    def __init__(self, AB, kl, ku, ipiv, info):
-        self.AB, self.kl, self.ku, self.ipiv, self.info = AB, kl, ku, ipiv, info
-
-    def solve(self, B):
-        return band_getrs(self.AB, self.kl, self.ku, self.ipiv, B)
-
-
-def structure_aware_lu(A, kl_cap=-1, ku_cap=-1):
-    """Listing 2 on the GPU: detect, and if the speedup constraint holds,
-    convert and factor with the banded LU; otherwise factor densely.
-
-    Returns ("banded", BandLU) or ("dense", (LU, pivots)) where the dense
-    branch is the generic algorithm F (rocSOLVER getrf via torch).
-    """
-    out = band_detect(A, kl_cap, ku_cap)
-    kl, ku, exceeded = (int(v) for v in out.cpu())  # the one device->host copy
-    n = A.shape[0]
-    if not exceeded and speedup_predicate(n, kl, ku):
-        AB = dense_to_band(A, kl, ku)
-        ipiv, info = band_getrf(AB, kl, ku)
-        return "banded", BandLU(AB, kl, ku, ipiv, info)
-    return "dense", torch.linalg.lu_factor(A[:, :n].transpose(0, 1))

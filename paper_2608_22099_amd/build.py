@@ -1,6 +1,6 @@
 """Build libbandlu.so (gfx950 only) from csrc/*.hip with hipcc.
 
-Usage: python -m paper_2608_22099_amd.build [-j N]
+Usage: python -m paper_2608_22099_amd.build [-j N] [--incremental]
 
 Every translation unit is compiled for gfx950 with IEEE-exact floating point
 (no fast-math, no fp contraction: every fused multiply-add in the kernels is
@@ -38,8 +38,18 @@ def sources():
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 
-def _compile(src):
+def _headers_mtime():
+    hs = [os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hpp")]
+    hs += [os.path.join(INCLUDE, f) for f in os.listdir(INCLUDE) if f.endswith(".h")]
+    return max((os.path.getmtime(h) for h in hs), default=0.0)
+
+
+def _compile(src, incremental=False, hdr_mtime=0.0):
     obj = os.path.join(BUILD, os.path.basename(src)[:-4] + ".o")
+    if incremental and os.path.exists(obj):
+        t = os.path.getmtime(obj)
+        if t >= os.path.getmtime(src) and t >= hdr_mtime:
+            return obj, ""
     cmd = [HIPCC, *CFLAGS, "-Rpass-analysis=kernel-resource-usage", "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
@@ -61,13 +71,16 @@ def _compile(src):
     return obj, err
 
 
-def build(jobs: int | None = None, verbose: bool = False) -> str:
+def build(jobs: int | None = None, verbose: bool = False, incremental: bool = False) -> str:
+    """Compile every source (or, with incremental, only those whose object is
+    older than the source or any header) and link the library."""
     os.makedirs(BUILD, exist_ok=True)
     srcs = sources()
     jobs = jobs or min(len(srcs), max(1, (os.cpu_count() or 4)))
     objs = []
+    hdr = _headers_mtime()
     with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
-        for obj, err in ex.map(_compile, srcs):
+        for obj, err in ex.map(lambda f: _compile(f, incremental, hdr), srcs):
             objs.append(obj)
             if verbose and err.strip():
                 print(err, file=sys.stderr)
@@ -84,5 +97,7 @@ if __name__ == "__main__":
     ap = argparse.ArgumentParser()
     ap.add_argument("-j", type=int, default=None)
     ap.add_argument("-v", action="store_true")
+    ap.add_argument("--incremental", action="store_true",
+                    help="recompile only sources older than their object")
     a = ap.parse_args()
-    print(build(a.j, a.v))
+    print(build(a.j, a.v, a.incremental))

@@ -256,7 +256,19 @@ int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
     int v = variant;
     if (v == 0) {
         v = select_variant(n, kl, ku, batch);
-        if (!variant_fits(v, n, kl, ku, ldab, batch)) v = BANDLU_GETRF_GENERIC;
+        if (!variant_fits(v, n, kl, ku, ldab, batch)) {
+            // the caller's ldab (or stride) rules out the kernel chosen from the
+            // sizes alone: take the next kernel in the order of preference that
+            // fits, the one-workgroup kernel last
+            const int chain[] = {BANDLU_GETRF_WINDOW_G16, BANDLU_GETRF_DIAG, BANDLU_GETRF_SPLIT,
+                                 BANDLU_GETRF_WINDOW,
+                                 kl >= 32 ? BANDLU_GETRF_BLOCKED_MFMA : BANDLU_GETRF_BLOCKED};
+            int k = 0;
+            while (k < 5 && chain[k] != v) ++k;
+            v = BANDLU_GETRF_GENERIC;
+            for (++k; k < 5; ++k)
+                if (variant_fits(chain[k], n, kl, ku, ldab, batch)) { v = chain[k]; break; }
+        }
     } else if (!variant_fits(v, n, kl, ku, ldab, batch)) {
         set_error("band_getrf: variant %d cannot factor n = %lld, kl = %lld, ku = %lld", v,
                   (long long)n, (long long)kl, (long long)ku);

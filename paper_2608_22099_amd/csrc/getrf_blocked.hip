@@ -6,9 +6,10 @@
 // j0 + NB - 1 + kl + ku) in blocks of 32 columns, one workgroup per block and
 // one thread per band row, the row's 32 entries held in registers:
 //   phase A: the block receives panel k-1's row interchanges and rank-1
-//            updates one step after another, in the unblocked order, so every
-//            entry sees the same fused multiply-adds as in the unblocked
-//            algorithm;
+//            updates one step after another, in the unblocked order and over
+//            the same columns (up to the update extent ju of each step, none
+//            for a zero pivot), so every entry sees the same fused
+//            multiply-adds as in the unblocked algorithm;
 //   phase B: workgroup 0's block is panel k itself (its rows below panel
 //            k-1's reach were loaded too); it is factored in place with
 //            partial pivoting while the other workgroups finish their blocks.
@@ -90,6 +91,9 @@ __global__ __launch_bounds__(kRows) void blk_step_kernel(StepParams P) {
     __shared__ int s_idx[kRows / 64];
     __shared__ double s_val[kRows / 64];
     __shared__ int s_piv[NB];
+    __shared__ int s_nz[NB];   // applied panel: pivot of the step is nonzero
+    __shared__ int s_ju[NB];   // applied panel: update extent of the step
+    __shared__ int s_jub;      // factored panel: update extent before it
 
     double x[NBC];
     unsigned okx = 0;
@@ -105,9 +109,30 @@ __global__ __launch_bounds__(kRows) void blk_step_kernel(StepParams P) {
     int step = 0;  // parity of the LDS row buffers
 
     // ---------------------------------------------------------- phase A --
+    // Update extent (xGBTRF's ju): step j updates columns j+1..ju_j with
+    // ju_j = max(ju_{j-1}, min(j+ku+p_j, n-1)) over the steps with a nonzero
+    // pivot.  At such a step ju_j equals the maximum of min(s+ku+p_s, n-1) over
+    // s = j-kl..j whatever the pivots of those s were: a step s < j-kl reaches
+    // at most s+kl+ku < j+ku, and a zero-pivot step s < j has p_s = 0 and
+    // reaches s+ku < j+ku.  So the extent follows from the last kl+1 pivots.
+    auto reach = [&](int s) -> int {
+        return s < 0 ? 0 : min(s + ku + (ipiv[s] - 1 - s), n - 1);
+    };
     if (upd) {
-        // the panel's pivots, staged once
-        if (t < nb) s_piv[t] = ipiv[j0 + t] - 1 - (j0 + t);
+        // the panel's pivots, staged once, with each step's extent and whether
+        // its pivot (the final diagonal entry) is nonzero
+        __shared__ int s_c[kRows];
+        if (t < kl + nb) s_c[t] = reach(j0 - kl + t);
+        if (t < nb) {
+            s_piv[t] = ipiv[j0 + t] - 1 - (j0 + t);
+            s_nz[t] = AB[int64_t(j0 + t) * ldab + kv] != 0.0;
+        }
+        lds_barrier();
+        if (t < nb) {
+            int m = 0;
+            for (int u = 0; u <= kl + t; ++u) m = max(m, s_c[u]);
+            s_ju[t] = m;
+        }
         // multiplier of panel column jj for this thread's row, loaded 4 steps
         // ahead (only used by rows that have one: no need to clear the others)
         auto lval = [&](int jj) -> double {
@@ -129,6 +154,8 @@ __global__ __launch_bounds__(kRows) void blk_step_kernel(StepParams P) {
                     const int j = j0 + jj;
                     const int p = s_piv[jj];
                     const int km = min(kl, n - 1 - j);
+                    const bool nz = s_nz[jj] != 0;
+                    const int ncol = s_ju[jj] - cb;  // block columns c < ncol are within ju
                     const double l = lr[q];
                     lr[q] = lval(jj + 4);
                     const int A = step & 1;
@@ -142,16 +169,18 @@ __global__ __launch_bounds__(kRows) void blk_step_kernel(StepParams P) {
                         for (int c = 0; c < NBC; ++c) T2[A][c] = x[c];
                     }
                     lds_barrier();
+                    // (a zero pivot has p = 0: no interchange and no update)
                     if (t == jj) {
 #pragma unroll
-                        for (int c = 0; c < NBC; ++c) x[c] = S[A][c];
+                        for (int c = 0; c < NBC; ++c) if (c <= ncol) x[c] = S[A][c];
                     } else if (p != 0 && t == jj + p) {
 #pragma unroll
-                        for (int c = 0; c < NBC; ++c) x[c] = T2[A][c];
+                        for (int c = 0; c < NBC; ++c) if (c <= ncol) x[c] = T2[A][c];
                     }
-                    if (t > jj && t - jj <= km) {
+                    if (nz && t > jj && t - jj <= km) {
 #pragma unroll
-                        for (int c = 0; c < NBC; ++c) x[c] = __builtin_fma(-l, S[A][c], x[c]);
+                        for (int c = 0; c < NBC; ++c)
+                            if (c <= ncol) x[c] = __builtin_fma(-l, S[A][c], x[c]);
                     }
                 }
             }
@@ -161,6 +190,12 @@ __global__ __launch_bounds__(kRows) void blk_step_kernel(StepParams P) {
     if (fac) {
         const int off = upd ? nb : 0;  // thread index of row jn
         int info = 0;
+        // extent before the panel, from the kl steps before it
+        if (t == 0) s_jub = 0;
+        lds_barrier();
+        if (t < kl && jn - 1 - t >= 0) atomicMax(&s_jub, reach(jn - 1 - t));
+        lds_barrier();
+        int ju = s_jub;
 #pragma unroll
         for (int jj = 0; jj < NB; ++jj) {
             if (jj < nbn) {
@@ -198,6 +233,8 @@ __global__ __launch_bounds__(kRows) void blk_step_kernel(StepParams P) {
                 const int A = step & 1;
                 ++step;
                 if (bv != 0.0) {
+                    ju = max(ju, min(j + ku + p, n - 1));
+                    const int ncol = ju - cb;
                     if (t == off + jj + p) {
 #pragma unroll
                         for (int c = 0; c < NBC; ++c) S[A][c] = x[c];
@@ -211,18 +248,18 @@ __global__ __launch_bounds__(kRows) void blk_step_kernel(StepParams P) {
                     // keep their multipliers (product form of L)
                     if (t == off + jj) {
 #pragma unroll
-                        for (int c = 0; c < NBC; ++c) if (c >= jj) x[c] = S[A][c];
+                        for (int c = jj; c < NBC; ++c) x[c] = c <= ncol ? S[A][c] : x[c];
                     } else if (p != 0 && t == off + jj + p) {
 #pragma unroll
-                        for (int c = 0; c < NBC; ++c) if (c >= jj) x[c] = T2[A][c];
+                        for (int c = jj; c < NBC; ++c) x[c] = c <= ncol ? T2[A][c] : x[c];
                     }
                     const double piv = S[A][jj];
                     if (tt >= 1 && tt <= km && own) {
                         const double l = fabs(piv) >= DBL_MIN ? x[jj] * (1.0 / piv) : x[jj] / piv;
                         x[jj] = l;
 #pragma unroll
-                        for (int c = 0; c < NBC; ++c)
-                            if (c > jj) x[c] = __builtin_fma(-l, S[A][c], x[c]);
+                        for (int c = jj + 1; c < NBC; ++c)
+                            x[c] = c <= ncol ? __builtin_fma(-l, S[A][c], x[c]) : x[c];
                     }
                 } else {
                     if (info == 0) info = j + 1;

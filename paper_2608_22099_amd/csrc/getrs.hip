@@ -440,6 +440,60 @@ __global__ __launch_bounds__(64) void getrs_g16_kernel(RsParams P, int64_t syste
     }
 }
 
+// Any band: one workgroup of 256 threads per right-hand side, the vector in
+// LDS when it fits (else updated in place in global memory), two barriers per
+// step.  Each entry receives its fused multiply-adds in the order of the
+// sequence above, so the result is bitwise that of the narrower kernels.
+constexpr int kAnyThreads = 256;
+
+template <bool LDS>
+__global__ __launch_bounds__(kAnyThreads) void getrs_any_kernel(RsParams P) {
+    extern __shared__ double smem[];
+    const int64_t sys = blockIdx.x;
+    const int64_t b = sys / P.nrhs, k = sys - b * P.nrhs;
+    const double *__restrict__ AB = P.AB + b * P.strideAB;
+    const int32_t *__restrict__ ipiv = P.ipiv + b * P.strideP;
+    double *Bg = P.B + b * P.strideB + k * P.ldb;
+    double *x = LDS ? smem : Bg;
+    const int tid = threadIdx.x;
+    const int64_t n = P.n, kl = P.kl, kv = P.kl + P.ku, ldab = P.ldab;
+    if (LDS) {
+        for (int64_t i = tid; i < n; i += kAnyThreads) x[i] = Bg[i];
+    }
+    __syncthreads();
+    if (kl > 0) {
+        for (int64_t j = 0; j < n - 1; ++j) {
+            const int64_t km = min(kl, n - 1 - j);
+            if (tid == 0) {
+                const int64_t l = ipiv[j] - 1;
+                if (l != j && l > j && l < n) {
+                    const double t0 = x[l];
+                    x[l] = x[j];
+                    x[j] = t0;
+                }
+            }
+            __syncthreads();
+            const double xj = x[j];
+            const double *lc = AB + j * ldab + kv;
+            for (int64_t t = 1 + tid; t <= km; t += kAnyThreads)
+                x[j + t] = __builtin_fma(-lc[t], xj, x[j + t]);
+            __syncthreads();
+        }
+    }
+    for (int64_t j = n - 1; j >= 0; --j) {
+        const double *uc = AB + j * ldab + kv - j;  // uc[i] = U(i, j)
+        if (tid == 0) x[j] = x[j] / uc[j];
+        __syncthreads();
+        const double xj = x[j];
+        for (int64_t i = max(int64_t(0), j - kv) + tid; i < j; i += kAnyThreads)
+            x[i] = __builtin_fma(-uc[i], xj, x[i]);
+        __syncthreads();
+    }
+    if (LDS) {
+        for (int64_t i = tid; i < n; i += kAnyThreads) Bg[i] = x[i];
+    }
+}
+
 template <int W>
 constexpr int rs_depth() { return W >= 16 ? 2 : 32 / W; }
 
@@ -546,8 +600,15 @@ int launch_getrs(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *
     if (lanes_needed <= 256) return launch_w<4>(lds, P, systems, s);
     if (lanes_needed <= 512) return launch_w<8>(lds, P, systems, s);
     if (lanes_needed <= 1024) return launch_w<16>(lds, P, systems, s);
-    set_error("band_getrs: kl + ku + 1 > 1024 is not supported");
-    return BANDLU_ERR_UNSUPPORTED;
+    if (lds) {
+        hipLaunchKernelGGL(getrs_any_kernel<true>, dim3((unsigned)systems), dim3(kAnyThreads),
+                           size_t(n) * sizeof(double), s, P);
+    } else {
+        hipLaunchKernelGGL(getrs_any_kernel<false>, dim3((unsigned)systems), dim3(kAnyThreads), 0,
+                           s, P);
+    }
+    BANDLU_CHECK_LAUNCH("band_getrs (any band)");
+    return BANDLU_OK;
 }
 
 }  // namespace

@@ -63,7 +63,10 @@ def banded_dense(n, kl, ku, seed, dist="normal", shift=0.0, out=None, check=True
     it is zeroed first.  Returns the (n, lda) array.
     """
     if out is None:
-        out = np.zeros((n, n), dtype=np.float64)
+        # zeroed by one sequential pass: pages touched first by the scattered
+        # band writes below are far slower to map than pages touched in order
+        out = np.empty((n, n), dtype=np.float64)
+        out.fill(0.0)
     else:
         if out.shape[0] != n or out.shape[1] < n or out.dtype != np.float64:
             raise ValueError("out must be float64 of shape (n, lda >= n)")

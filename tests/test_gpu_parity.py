@@ -790,3 +790,114 @@ def test_getrf_mfma_deterministic():
     a = gpu_pipeline(T, 64, 64)
     b = gpu_pipeline(T, 64, 64)
     assert_bitwise(a[1], b[1], "rerun")
+
+
+# ---------------------------------------------------- one-workgroup getrf --
+def special_band(n, kl, ku, seed, neg_zero=0.0, nans=0, zero_cols=()):
+    """A random band with in-band -0.0 entries (fraction neg_zero), a few NaNs
+    and zeroed columns: the inputs where only the exact update extent keeps a
+    kernel bitwise equal to the unblocked algorithm."""
+    T = random_band(n, kl, ku, seed)
+    rng = np.random.default_rng(seed + 1)
+    j, i = inputs.band_index(n, kl, ku)
+    if neg_zero:
+        pick = rng.random(j.size) < neg_zero
+        T[j[pick], i[pick]] = -0.0
+    for q in rng.choice(j.size, size=min(nans, j.size), replace=False) if nans else ():
+        T[j[q], i[q]] = np.nan
+    for c in zero_cols:
+        T[c, :] = 0.0
+    return T
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_getrf_generic_forced(seed):
+    """The one-workgroup kernel (the default beyond kl = 256) forced on random
+    shapes, with -0.0 entries, NaNs and singular columns: bitwise."""
+    rng = np.random.default_rng(7000 + seed)
+    n = int(rng.integers(1, 160))
+    kl, ku = int(rng.integers(0, n)), int(rng.integers(0, n))
+    T = special_band(n, kl, ku, 7100 + seed, neg_zero=0.2 if seed % 2 else 0.0,
+                     nans=seed % 3, zero_cols=(n // 2,) if seed % 4 == 1 else ())
+    g = gpu_pipeline(T, kl, ku, variant="generic")
+    o = oracle_pipeline(T, kl, ku)
+    assert np.array_equal(g[2], o[2]) and g[3] == o[3]
+    assert_bitwise(g[1], o[1], f"generic n={n} kl={kl} ku={ku}")
+
+
+@pytest.mark.parametrize("n,kl,ku", [(600, 300, 20), (400, 399, 0), (700, 257, 257)])
+def test_getrf_generic_default(n, kl, ku):
+    """kl > 256 runs the one-workgroup kernel by default."""
+    assert bandlu.band_getrf_variant(n, kl, ku) == "generic"
+    for zero in (None, n // 3):
+        T = special_band(n, kl, ku, 7300 + n, neg_zero=0.05, zero_cols=() if zero is None else (zero,))
+        g, o = gpu_pipeline(T, kl, ku), oracle_pipeline(T, kl, ku)
+        assert np.array_equal(g[2], o[2]) and g[3] == o[3]
+        assert_bitwise(g[1], o[1], f"generic default n={n} kl={kl} ku={ku} zero col {zero}")
+
+
+# A leading dimension above 2kl+ku+1 must neither change the result nor send
+# the call to a slower kernel than needed (the choice falls back through the
+# kernels that fit before the one-workgroup kernel).
+@pytest.mark.parametrize("n,kl,ku,pad,shift", [(500, 3, 5, 1, 20.0), (500, 3, 5, 7, 0.0),
+                                               (400, 16, 16, 1, 0.0), (300, 16, 16, 3, 40.0),
+                                               (300, 0, 10, 2, 0.0), (300, 2, 64, 5, 0.0),
+                                               (300, 20, 100, 4, 0.0), (200, 40, 30, 3, 0.0)])
+def test_getrf_padded_ldab(n, kl, ku, pad, shift):
+    ldab = 2 * kl + ku + 1 + pad
+    T = random_band(n, kl, ku, 8100 + n + kl + pad, shift=shift)
+    g = gpu_pipeline(T, kl, ku, ldab=ldab)
+    o = oracle_pipeline(T, kl, ku, ldab=ldab)
+    assert np.array_equal(g[2], o[2]) and g[3] == o[3]
+    what = f"padded ldab={ldab} n={n} kl={kl} ku={ku}"
+    if kl >= 32:
+        assert_factors_close(g[1][:, :ldab - pad], o[1][:, :ldab - pad], kl, ku, what)
+    else:
+        assert_bitwise(g[1][:, :ldab - pad], o[1][:, :ldab - pad], what)
+    # rows beyond 2kl+ku are never written
+    assert_bitwise(g[1][:, ldab - pad:], g[0][:, ldab - pad:], what + " (padding rows)",
+                   nan_payload=True)
+
+
+def test_getrf_padded_ldab_batched():
+    batch, n, kl, ku = 70, 64, 4, 4
+    ldab = 2 * kl + ku + 1 + 3
+    T = np.stack([random_band(n, kl, ku, 8200 + b) for b in range(batch)])
+    AB = torch.zeros((batch, n, ldab), dtype=torch.float64, device=DEV)
+    bandlu.dense_to_band_batched(to_dev(T), kl, ku, AB=AB)
+    ipiv, info = bandlu.band_getrf_batched(AB, kl, ku)
+    ABg, ipg, infg = AB.cpu().numpy(), ipiv.cpu().numpy(), info.cpu().numpy()
+    for b in range(batch):
+        o = oracle_pipeline(T[b], kl, ku, ldab=ldab)
+        assert np.array_equal(ipg[b], o[2]) and infg[b] == o[3], b
+        assert_bitwise(ABg[b], o[1], f"batch {b}")
+
+
+@pytest.mark.parametrize("n,kl,ku", [(300, 20, 100), (200, 5, 120), (300, 40, 3), (500, 31, 90)])
+def test_getrf_blocked_special_values(n, kl, ku):
+    """The blocked kernel applies each step only up to the step's update
+    extent and skips zero pivots, as the unblocked algorithm does, so in-band
+    -0.0 entries, NaNs and zero columns come out bitwise the same."""
+    for k, (nz, nans, zc) in enumerate([(0.3, 0, ()), (0.1, 2, ()), (0.2, 0, (n // 3, n // 3 + 1))]):
+        T = special_band(n, kl, ku, 8300 + n + k, neg_zero=nz, nans=nans, zero_cols=zc)
+        g = gpu_pipeline(T, kl, ku, variant="blocked")
+        o = oracle_pipeline(T, kl, ku)
+        assert np.array_equal(g[2], o[2]) and g[3] == o[3]
+        assert_bitwise(g[1], o[1], f"blocked specials n={n} kl={kl} ku={ku} case {k}")
+
+
+# ------------------------------------------------------ any-band solve --
+@pytest.mark.parametrize("n,kl,ku,nrhs", [(1500, 600, 500, 2), (8300, 10, 1020, 1), (1100, 1000, 90, 1)])
+def test_getrs_any_band(n, kl, ku, nrhs):
+    """kl+ku+1 > 1024: the any-band solve, with the right-hand sides in LDS
+    (n <= 8192) and in global memory, bitwise."""
+    T = random_band(n, kl, ku, 8400 + n, shift=float(kl + ku))
+    o = oracle_pipeline(T, kl, ku)
+    B = np.random.default_rng(n).standard_normal((nrhs, n))
+    Bg = to_dev(B)
+    bandlu.band_getrs(to_dev(o[1]), kl, ku, to_dev(o[2]), Bg)
+    xo = oracle.gbtrs(o[1], kl, ku, o[2], B.copy())
+    assert_bitwise(Bg.cpu().numpy(), xo, f"any-band getrs n={n} kl={kl} ku={ku}")
+    Bg = to_dev(B)
+    bandlu.band_getrs(to_dev(o[1]), kl, ku, to_dev(o[2]), Bg, variant="generic")
+    assert_bitwise(Bg.cpu().numpy(), xo, "forced generic")

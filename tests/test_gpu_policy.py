@@ -1,0 +1,115 @@
+"""Listing 2 end to end on the GPU (structure_aware_lu): detection with the
+early-exit caps of the speedup constraint, the one device-to-host copy, and
+then either the banded branch (convert + band LU, compared with the oracle bit
+for bit) or the dense branch (rocSOLVER getrf through torch, checked by its
+backward error).  Also the cost model measured on the device and the slowdown
+experiment of Sec. II-B on dense inputs."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_22099_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from paper_2608_22099_amd import bandlu, policy  # noqa: E402
+
+DEV = "cuda:0"
+
+
+def bits(x):
+    return np.ascontiguousarray(x).view(np.uint64)
+
+
+@pytest.mark.parametrize("name", ["n1000_kl3_ku3", "n8192_kl16_ku16", "n16384_kl2_ku64"])
+def test_structure_aware_lu_banded(name):
+    w = inputs.WORKLOADS[name]
+    n, kl, ku = w["n"], w["kl"], w["ku"]
+    T = inputs.workload_matrix(name)
+    A = torch.from_numpy(T).to(DEV)
+    res = policy.structure_aware_lu(A)
+    assert res.branch == "banded" and (res.kl, res.ku) == (kl, ku)
+    ABo, _ = oracle.dense_to_band(T, kl, ku)
+    ipo, info_o, _ = oracle.gbtrf(ABo, kl, ku)
+    assert np.array_equal(res.ipiv.cpu().numpy(), ipo)
+    assert int(res.info.cpu()[0]) == info_o
+    assert np.array_equal(bits(res.AB.cpu().numpy()), bits(ABo))
+    b = inputs.workload_rhs(name)
+    x = res.solve(torch.from_numpy(b.copy()).to(DEV))
+    xo = oracle.gbtrs(ABo, kl, ku, ipo, b.copy())
+    assert np.array_equal(bits(x.cpu().numpy()), bits(xo))
+
+
+def dense_backward_error(T, res):
+    n = T.shape[0]
+    A = T[:, :n].T
+    LU = res.LU.cpu().numpy()
+    piv = res.pivots.cpu().numpy()
+    L = np.tril(LU, -1) + np.eye(n)
+    U = np.triu(LU)
+    P = np.eye(n)
+    for k in range(n):
+        q = piv[k] - 1
+        P[[k, q]] = P[[q, k]]
+    return np.linalg.norm(P @ A - L @ U) / (np.linalg.norm(A) * n * np.finfo(float).eps)
+
+
+def test_dense_input_takes_dense_branch():
+    """A dense N(0,1) matrix: detection stops early (a bandwidth passes its
+    cap) and the generic LU runs."""
+    n = 700
+    T = np.random.default_rng(12).standard_normal((n, n))
+    res = policy.structure_aware_lu(torch.from_numpy(T).to(DEV))
+    assert res.branch == "dense" and res.exceeded == 1
+    assert dense_backward_error(T, res) <= 10.0
+    b = np.random.default_rng(13).standard_normal((1, n))
+    x = res.solve(torch.from_numpy(b.copy()).to(DEV)).cpu().numpy()[0]
+    A = T.T
+    r = np.abs(A @ x - b[0]).max() / (np.abs(A).sum(1).max() * np.abs(x).max() * n * np.finfo(float).eps)
+    assert r <= 10.0
+
+
+def test_capped_band_takes_dense_branch():
+    """A band wider than the caller's caps goes to the dense branch."""
+    n, kl, ku = 2048, 16, 16
+    T = inputs.banded_dense(n, kl, ku, 99, shift=64.0)
+    res = policy.structure_aware_lu(torch.from_numpy(T).to(DEV), caps=(8, 8))
+    assert res.branch == "dense" and res.exceeded == 1
+    assert dense_backward_error(T, res) <= 10.0
+
+
+def test_band_failing_the_constraint_takes_dense_branch():
+    """Bandwidths within no cap, but too wide for the banded LU to pay
+    (I + C + f >= F): detected exactly, then factored densely."""
+    n, kl, ku = 300, 200, 200
+    assert not policy.speedup_predicate(n, kl, ku)
+    T = inputs.banded_dense(n, kl, ku, 5)
+    res = policy.structure_aware_lu(torch.from_numpy(T).to(DEV), caps=(-1, -1))
+    assert res.branch == "dense" and res.exceeded == 0 and (res.kl, res.ku) == (kl, ku)
+    assert dense_backward_error(T, res) <= 10.0
+
+
+def test_cost_model_and_slowdown():
+    model = policy.CostModel.measure(DEV)
+    d = model.as_dict()
+    assert d["detect_GBs"] > 100 and d["convert_GBs"] > 10 and model.dense_b > 0
+    print("cost model:", d)
+    for name in ("n8192_kl16_ku16", "n16384_kl2_ku64", "n32768_kl256_ku256"):
+        w = inputs.WORKLOADS[name]
+        assert policy.speedup_predicate(w["n"], w["kl"], w["ku"], model), name
+    n = 8192
+    assert policy.slowdown_constraint(n, model)
+    kl_cap, ku_cap = policy.band_caps(n, model)
+    assert 0 <= kl_cap < n - 1
+    assert not policy.speedup_predicate(n, kl_cap + 1, 0, model)
+    A = torch.randn((2048, 2048), dtype=torch.float64, device=DEV,
+                    generator=torch.Generator(device=DEV).manual_seed(3))
+    s = policy.timed_slowdown(A, model)
+    assert s["detect_capped_result"][2] == 1
+    assert 1.0 <= s["slowdown"] <= s["slowdown_full_scan"] + 0.05
+    res = policy.structure_aware_lu(A, model=model)
+    assert res.branch == "dense"

@@ -61,24 +61,25 @@ def test_batched_workload():
     out, dmax = bandlu.band_detect_batched(A)
     out = out.cpu().numpy()
     assert tuple(dmax.cpu().numpy()) == (kl, ku, 0)
-    sample = list(range(0, batch, 97)) + [batch - 1]
-    for b in sample:
-        assert tuple(out[b]) == oracle.detect(T[b])[:3]
     AB = bandlu.dense_to_band_batched(A, kl, ku)
     del A
+    AB0g = AB.cpu().numpy()
     ipiv, info = bandlu.band_getrf_batched(AB, kl, ku)
     B = np.stack([inputs.workload_rhs(name, b) for b in range(batch)])
     Bg = torch.from_numpy(B).to(DEV)
     bandlu.band_getrs_batched(AB, kl, ku, ipiv, Bg)
     ABg, ipg, infg, xg = AB.cpu().numpy(), ipiv.cpu().numpy(), info.cpu().numpy(), Bg.cpu().numpy()
-    assert np.all(infg == 0)
-    for b in sample:
+    # every matrix of the batch, every output, bit for bit
+    for b in range(batch):
+        assert tuple(out[b]) == oracle.detect(T[b])[:3], b
         ABo, _ = oracle.dense_to_band(T[b], kl, ku)
+        assert np.array_equal(bits(AB0g[b]), bits(ABo)), b
         ipo, info_o, _ = oracle.gbtrf(ABo, kl, ku)
-        assert np.array_equal(ipg[b], ipo)
-        assert np.array_equal(bits(ABg[b]), bits(ABo))
+        assert infg[b] == info_o, b
+        assert np.array_equal(ipg[b], ipo), b
+        assert np.array_equal(bits(ABg[b]), bits(ABo)), b
         xo = oracle.gbtrs(ABo, kl, ku, ipo, B[b].copy())
-        assert np.array_equal(bits(xg[b]), bits(xo))
+        assert np.array_equal(bits(xg[b]), bits(xo)), b
 
 
 def test_wide_band_workload():

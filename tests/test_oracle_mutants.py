@@ -25,6 +25,12 @@ MUTANTS = {
     "scale_by_division": ("AT(j + t, j) = AT(j + t, j) * r;", "AT(j + t, j) = AT(j + t, j) / piv;"),
     "info_index": ("*info = (int32_t)(j + 1);\n        }\n    }\n#undef AT\n    if (flops)",
                    "*info = (int32_t)(j);\n        }\n    }\n#undef AT\n    if (flops)"),
+    "tiny_pivot_reciprocal": ("for (int64_t t = 1; t <= km; ++t) AT(j + t, j) = AT(j + t, j) / piv;",
+                              "for (int64_t t = 1; t <= km; ++t) AT(j + t, j) = AT(j + t, j) * (1.0 / piv);"),
+    "gepp_tiny_pivot_reciprocal": ("for (int64_t i = k + 1; i < n; ++i) A[i + k * lda] /= piv;",
+                                   "for (int64_t i = k + 1; i < n; ++i) A[i + k * lda] *= 1.0 / piv;"),
+    "tiny_pivot_threshold": ("if (fabs(piv) >= DBL_MIN) {\n                    double r = 1.0 / piv;",
+                             "if (fabs(piv) > 0.0) {\n                    double r = 1.0 / piv;"),
     "fill_zeroing": ("r < kl; ++r) AB[r + c * ldab] = 0.0;", "r < kl; ++r) (void)0;"),
 }
 

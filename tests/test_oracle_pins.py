@@ -291,6 +291,35 @@ class TestBandLU:
         assert info == 1 and np.array_equal(ipiv, np.arange(1, 6))
         assert np.all(AB == 0.0)
 
+    def test_subnormal_pivot_divides(self):
+        """A pivot below DBL_MIN is divided into the column instead of being
+        inverted (1/p would overflow to Inf).  The multipliers and the Schur
+        complement are exact by hand: 2t/4t = 0.5, 3 - 0.5*2 = 2, and t/3t is
+        the correctly rounded 1/3 (t = 2^-1074, the smallest subnormal).
+        Checked on the band routine and on the dense brute force."""
+        t = math.ldexp(1.0, -1074)
+        third = np.array([0x3FD5555555555555], dtype=np.uint64).view(np.float64)[0]
+        for p, a, l_want, u22_want in [(4 * t, 2 * t, 0.5, 2.0), (3 * t, t, third, 3.0 - third * 2.0)]:
+            assert 0.0 < p < np.finfo(float).tiny
+            A = np.array([[p, 2.0], [a, 3.0]])
+            T = np.ascontiguousarray(A.T)
+            _, AB, ipiv, info, _ = band_lu(T, 1, 1)
+            assert info == 0 and list(ipiv) == [1, 2]
+            assert AB[0, 3] == l_want and bits(AB[0, 3:4])[0] == bits(np.array([l_want]))[0]
+            assert AB[1, 2] == u22_want
+            assert AB[0, 2] == p and AB[1, 1] == 2.0
+            D = T.copy()
+            dpiv, dinfo = oracle.dense_gepp(D)
+            assert dinfo == 0 and list(dpiv) == [1, 2]
+            assert D[0, 1] == l_want and D[1, 1] == u22_want
+        # a pivot exactly at DBL_MIN is inverted (2^1022 is finite): 1/DBL_MIN
+        # times DBL_MIN/2 is exactly 0.5 either way, and the branch boundary
+        # must not send it to Inf
+        m = np.finfo(float).tiny
+        T = np.ascontiguousarray(np.array([[m, 1.0], [m / 2, 1.0]]).T)
+        _, AB, ipiv, info, _ = band_lu(T, 1, 1)
+        assert AB[0, 3] == 0.5 and AB[1, 2] == 0.5
+
     def test_nan_pivot_convention(self):
         """i_amax: a NaN in first position is taken, later NaNs are never taken."""
         A = np.array([[np.nan, 1.0], [3.0, 1.0]])
