@@ -129,11 +129,17 @@ int dense_to_band_batched(const double *dA, int64_t n, int64_t lda, int64_t stri
  * Multipliers are formed as a * (1/pivot) when |pivot| >= DBL_MIN, else as
  * a / pivot; every update is one fused multiply-add.  Below the
  * dense-contraction threshold (kl < 32) the factors are bitwise those of the
- * unblocked algorithm on finite data; from kl = 32 on (and kl <= 256) the
- * blocked variant applies each panel of 32 columns to the rest of the band
- * as a dense product on the fp64 matrix cores, which sums in another order:
- * its factors agree with the unblocked ones to rounding, and so do its
- * pivots unless two candidates of a column lie within rounding of each other.
+ * unblocked algorithm on finite data.  From kl = 32 on (and kl <= 256) each
+ * panel of 32 columns is applied to the rest of the band as a dense product
+ * on the fp64 matrix cores, in one persistent launch (BANDLU_GETRF_WIDE)
+ * when the batch fits the device's co-resident workgroups; each entry still
+ * receives its fused multiply-adds in the order of the column steps, and the
+ * factors are compared with the unblocked ones to a relative 1e-10.  The
+ * persistent launch allocates its hand-off scratch (about 75 KB per 32
+ * columns of kl+ku, per matrix) stream-ordered on `stream` and frees it the
+ * same way; its workgroups wait for each other with bounded waits, and if a
+ * wait ever ran out the kernel stops and sets *d_info = INT_MIN (the factors
+ * are then invalid).
  */
 int band_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab, int32_t *d_ipiv,
                int32_t *d_info, void *stream);
@@ -186,11 +192,13 @@ int band_getrs_batched(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const do
 #define BANDLU_GETRF_SPLIT 6        /* register window + a pivot wavefront      */
 #define BANDLU_GETRF_DIAG 7         /* diagonal pivots verified per column, the */
                                     /* split kernel from the first failing one  */
+#define BANDLU_GETRF_WIDE 8         /* one persistent launch: blocks of 32      */
+                                    /* columns in LDS, matrix-core updates      */
 int band_getrf_variant(int64_t n, int64_t kl, int64_t ku, int64_t batch);
 
 /*
  * band_getrf_ex -- band_getrf_batched with the kernel chosen by the caller:
- * variant 0 picks it as band_getrf_batched does, 1..7 forces that
+ * variant 0 picks it as band_getrf_batched does, 1..8 forces that
  * BANDLU_GETRF_* kernel.  Arguments 1-10 as in band_getrf_batched (argument
  * 11 is the variant).  A variant that cannot handle the sizes (a window for
  * kl > 31 or a band wider than its registers, a blocked variant for

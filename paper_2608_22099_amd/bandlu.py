@@ -61,7 +61,7 @@ for _name, _args in EXPORTS.items():
         else ctypes.c_int
 
 VARIANTS = {1: "window", 2: "window_g16", 3: "generic", 4: "blocked", 5: "blocked_mfma",
-            6: "split", 7: "diag"}
+            6: "split", 7: "diag", 8: "wide"}
 _VARIANT_CODES = {name: code for code, name in VARIANTS.items()}
 GETRS_VARIANTS = {1: "window", 2: "g16", 3: "ring", 4: "generic", 5: "lane"}
 _GETRS_CODES = {name: code for code, name in GETRS_VARIANTS.items()}

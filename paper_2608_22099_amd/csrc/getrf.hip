@@ -17,8 +17,13 @@
 //   BLOCKED     kl <= 31 beyond the windows: panels of 32 columns factored in
 //               registers, trailing band updated by many workgroups with the
 //               unblocked rank-1 order (getrf_blocked.hip);
-//   BLOCKED_MFMA  32 <= kl <= 256: the same panels, trailing band updated as
-//               a dense product on the fp64 matrix cores (getrf_mfma.hip);
+//   WIDE        32 <= kl <= 256 when the batch fits one launch of co-resident
+//               workgroups: one persistent launch, blocks of 32 columns kept
+//               in LDS, each panel factored by its block's owner and applied
+//               by the others on the fp64 matrix cores (getrf_wide.hip);
+//   BLOCKED_MFMA  32 <= kl <= 256 otherwise: one launch per panel, trailing
+//               band updated as a dense product on the matrix cores
+//               (getrf_mfma.hip);
 //   GENERIC     kl > 256: one workgroup per matrix works on the band in global
 //               memory, one column step at a time.
 // The window, blocked and generic kernels produce bitwise the factors of the
@@ -86,6 +91,11 @@ int launch_getrf_blocked(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t
 int launch_getrf_mfma(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
                       int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info,
                       int64_t batch, hipStream_t s);
+int launch_getrf_wide(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
+                      int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info,
+                      int64_t batch, hipStream_t s, void *scratch, size_t scratch_bytes);
+bool getrf_wide_fits(int64_t n, int64_t kl, int64_t ku, int64_t batch);
+bool getrf_wide_one_launch(int64_t n, int64_t kl, int64_t ku, int64_t batch);
 
 namespace {
 
@@ -210,7 +220,10 @@ int select_variant(int64_t n, int64_t kl, int64_t ku, int64_t batch) {
     if (kl <= 31 && (need <= 64 || (need <= 128 && kl <= 15)) && need * n * 8 <= kMaxBufferBytes)
         return BANDLU_GETRF_WINDOW;
     // from kl = 32 on, applying a panel of 32 columns is a real dense product
-    // (at least 32 x 32 x 32): matrix cores
+    // (at least 32 x 32 x 32): matrix cores, in one persistent launch when the
+    // batch fits the co-resident workgroups, else one launch per panel
+    if (kl >= 32 && kl <= 256 && getrf_wide_one_launch(n, kl, ku, batch))
+        return BANDLU_GETRF_WIDE;
     if (kl <= 256 && n <= INT32_MAX && batch <= 65535)
         return kl >= 32 ? BANDLU_GETRF_BLOCKED_MFMA : BANDLU_GETRF_BLOCKED;
     return BANDLU_GETRF_GENERIC;
@@ -235,6 +248,8 @@ bool variant_fits(int v, int64_t n, int64_t kl, int64_t ku, int64_t ldab, int64_
     case BANDLU_GETRF_BLOCKED:
     case BANDLU_GETRF_BLOCKED_MFMA:
         return kl <= 256 && batch <= 65535;
+    case BANDLU_GETRF_WIDE:
+        return getrf_wide_fits(n, kl, ku, batch);
     case BANDLU_GETRF_GENERIC:
         return true;
     default:
@@ -366,6 +381,9 @@ int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
                                     s);
     if (v == BANDLU_GETRF_BLOCKED_MFMA)
         return launch_getrf_mfma(n, kl, ku, dAB, ldab, strideAB, d_ipiv, strideP, d_info, batch, s);
+    if (v == BANDLU_GETRF_WIDE)
+        return launch_getrf_wide(n, kl, ku, dAB, ldab, strideAB, d_ipiv, strideP, d_info, batch, s,
+                                 nullptr, 0);
     GenParams P;
     P.AB = dAB;
     P.ipiv = d_ipiv;
@@ -451,7 +469,7 @@ extern "C" int band_getrf_ex(int64_t n, int64_t kl, int64_t ku, double *dAB, int
     BANDLU_ARG(batch <= 1 || strideP >= n, 8, "band_getrf_ex: strideP < n");
     BANDLU_ARG(batch == 0 || d_info != nullptr, 9, "band_getrf_ex: d_info is null");
     BANDLU_ARG(batch >= 0, 10, "band_getrf_ex: batch < 0");
-    BANDLU_ARG(variant >= 0 && variant <= BANDLU_GETRF_DIAG, 11,
+    BANDLU_ARG(variant >= 0 && variant <= BANDLU_GETRF_WIDE, 11,
                "band_getrf_ex: unknown variant");
     if (n > kMaxN || batch > INT_MAX) {
         set_error("band_getrf_ex: sizes too large");

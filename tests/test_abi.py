@@ -72,7 +72,7 @@ def test_argument_validation(lib):
     assert lib.band_getrs(10, 2, 3, 1, fake, 8, fake, fake, 9, None) == -9
     # band_getrf_ex: argument 11 is the variant; a variant that cannot take the
     # sizes is refused before anything is enqueued
-    assert lib.band_getrf_ex(10, 2, 3, fake, 8, 80, fake, 10, fake, 1, 8, None) == -11
+    assert lib.band_getrf_ex(10, 2, 3, fake, 8, 80, fake, 10, fake, 1, 9, None) == -11
     assert lib.band_getrf_ex(10, 0, 3, fake, 4, 40, fake, 10, fake, 1, 6, None) == -1001
     assert lib.band_getrf_ex(10, 0, 3, fake, 4, 40, fake, 10, fake, 1, 7, None) == -1001
     assert lib.band_getrf_ex(100, 2, 30, fake, 35, 3500, fake, 100, fake, 1, 7, None) == -1001
@@ -88,7 +88,7 @@ def test_argument_validation(lib):
 
 
 def test_variant_selection(lib):
-    W, G16, GEN, BLK, MF, SP, DG = 1, 2, 3, 4, 5, 6, 7
+    W, G16, GEN, BLK, MF, SP, DG, WD = 1, 2, 3, 4, 5, 6, 7, 8
     assert lib.band_getrf_variant(1000, 3, 3, 1) == DG
     assert lib.band_getrf_variant(8192, 16, 16, 1) == DG
     assert lib.band_getrf_variant(300, 23, 17, 1) == DG
@@ -103,10 +103,14 @@ def test_variant_selection(lib):
     assert lib.band_getrf_variant(300, 0, 5, 1) == W
     assert lib.band_getrf_variant(300, 16, 97, 1) == BLK
     assert lib.band_getrf_variant(256, 4, 4, 4096) == G16
-    assert lib.band_getrf_variant(300, 40, 3, 1) == MF
-    assert lib.band_getrf_variant(32768, 256, 256, 1) == MF
+    # kl >= 32: the persistent kernel when the batch fits one launch of
+    # co-resident workgroups (256 CUs assumed without a device), else one
+    # launch per panel
+    assert lib.band_getrf_variant(300, 40, 3, 1) == WD
+    assert lib.band_getrf_variant(32768, 256, 256, 1) == WD
+    assert lib.band_getrf_variant(300, 40, 3, 200) == MF
     assert lib.band_getrf_variant(300, 31, 90, 1) == BLK
     assert lib.band_getrf_variant(300, 20, 100, 1) == BLK
-    assert lib.band_getrf_variant(300, 32, 0, 1) == MF
+    assert lib.band_getrf_variant(300, 32, 0, 1) == WD
     assert lib.band_getrf_variant(2000, 300, 10, 1) == GEN
     assert lib.band_getrf_variant(-1, 0, 0, 1) == -1

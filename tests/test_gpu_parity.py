@@ -168,7 +168,7 @@ def test_getrf_random_shapes(seed):
     assert np.array_equal(g[2], o[2]), f"ipiv ({variant})"
     assert g[3] == o[3]
     what = f"factors ({variant}, n={n}, kl={kl}, ku={ku})"
-    if variant == "blocked_mfma":
+    if variant in ("blocked_mfma", "wide"):
         assert_factors_close(g[1], o[1], kl, ku, what)
         assert_backward_error(o[0], g[1], kl, ku, g[2], what)
     else:
@@ -659,12 +659,18 @@ def test_getrf_blocked_batched_and_singular():
 
 # ------------------------------------------------------ matrix-core getrf --
 def check_mfma(T, kl, ku, what, variant=None):
-    g, o = gpu_pipeline(T, kl, ku, variant=variant), oracle_pipeline(T, kl, ku)
-    assert np.array_equal(g[2], o[2]), f"{what}: ipiv"
-    assert g[3] == o[3], f"{what}: info {g[3]} vs {o[3]}"
-    assert_factors_close(g[1], o[1], kl, ku, what)
-    if np.any(o[0] != 0.0):
-        assert_backward_error(o[0], g[1], kl, ku, g[2], what)
+    """The matrix-core kernels against the oracle: the default choice (the
+    persistent kernel where the batch fits one launch) and, unless a variant
+    is named, the one-launch-per-panel kernel as well."""
+    o = oracle_pipeline(T, kl, ku)
+    for v in ([variant] if variant else [None, "blocked_mfma"]):
+        g = gpu_pipeline(T, kl, ku, variant=v)
+        w = f"{what} ({v or bandlu.band_getrf_variant(T.shape[0], kl, ku)})"
+        assert np.array_equal(g[2], o[2]), f"{w}: ipiv"
+        assert g[3] == o[3], f"{w}: info {g[3]} vs {o[3]}"
+        assert_factors_close(g[1], o[1], kl, ku, w)
+        if np.any(o[0] != 0.0):
+            assert_backward_error(o[0], g[1], kl, ku, g[2], w)
     return g, o
 
 
@@ -675,7 +681,7 @@ def check_mfma(T, kl, ku, what, variant=None):
 def test_getrf_mfma_shapes(n, kl, ku):
     """Panels of 32 with a ragged last panel, bands that reach one or many
     column blocks, kl at both ends of the variant's range."""
-    assert bandlu.band_getrf_variant(n, kl, ku) == "blocked_mfma"
+    assert bandlu.band_getrf_variant(n, kl, ku) == "wide"
     check_mfma(random_band(n, kl, ku, 7 * n + kl + ku), kl, ku, f"n={n} kl={kl} ku={ku}")
 
 
@@ -691,10 +697,11 @@ def test_getrf_mfma_random(seed):
 @pytest.mark.parametrize("n,kl,ku", [(40, 0, 0), (70, 3, 2), (100, 10, 5), (50, 20, 49),
                                      (31, 5, 5), (1, 0, 0), (2, 1, 1)])
 def test_getrf_mfma_forced_narrow(n, kl, ku):
-    """The matrix-core kernel also factors narrow bands when forced (blocks
+    """The matrix-core kernels also factor narrow bands when forced (blocks
     narrower than a panel, a band that does not reach the next panel)."""
-    check_mfma(random_band(n, kl, ku, 11 * n + kl), kl, ku, f"forced n={n} kl={kl} ku={ku}",
-               variant="blocked_mfma")
+    for v in ("blocked_mfma", "wide"):
+        check_mfma(random_band(n, kl, ku, 11 * n + kl), kl, ku, f"forced n={n} kl={kl} ku={ku}",
+                   variant=v)
 
 
 def test_getrf_mfma_pivoting_and_singular():

@@ -107,12 +107,15 @@ def test_wide_band_workload():
     b = inputs.workload_rhs(name)
     xo = oracle.gbtrs(ABo, kl, ku, ipo, b.copy())
 
-    assert bandlu.band_getrf_variant(n, kl, ku) == "blocked_mfma"
+    assert bandlu.band_getrf_variant(n, kl, ku) == "wide"
     ipiv, info = bandlu.band_getrf(AB, kl, ku)
     assert np.array_equal(ipiv.cpu().numpy(), ipo) and int(info.cpu()[0]) == 0
     ABg = AB.cpu().numpy()
     fallback = assert_factors_close(ABg, ABo, kl, ku, "matrix-core factors")
-    print(f"entries passing on the column scale: {fallback}")
+    differ = int(np.count_nonzero(bits(ABg) != bits(ABo)))
+    print(f"entries passing on the column scale: {fallback}; entries not bitwise equal: {differ}")
+    # every entry within the elementwise relative tolerance itself
+    assert fallback == 0
     assert_backward_error(AB0, ABg, kl, ku, ipiv.cpu().numpy(), "matrix-core factors")
     xg = torch.from_numpy(b.copy()).to(DEV)
     bandlu.band_getrs(AB, kl, ku, ipiv, xg)
