@@ -156,6 +156,33 @@ int band_getrf_batched(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t l
                        int64_t batch, void *stream);
 
 /*
+ * band_getrf_batched_noalloc -- band_getrf_batched for callers that cannot
+ * allocate device memory (code under stream capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Arguments, results and the kernel chosen
+ * are those of band_getrf_batched, and so the factors, ipiv and info are
+ * bitwise the same.  The caller still owns dAB, d_ipiv and d_info.  The one
+ * kernel that needs scratch, the persistent wide-band one, takes its
+ * hand-off ring from a fixed 16 MiB array that the library holds on each
+ * device it runs on until the process ends.  The function itself calls no
+ * hipMalloc, hipFree or other allocating routine.
+ *   - A matrix whose ring would exceed 16 MiB is rejected with
+ *     BANDLU_ERR_UNSUPPORTED before anything is enqueued.  Such a matrix has
+ *     kl >= 32 and kl+ku above about 7100; for kl = ku = 256 the ring is about
+ *     1.3 MB per matrix.
+ *   - A batch is factored in as many launches as the array needs, one after
+ *     another on `stream`.
+ *   - The first call on a device looks up the array's address on that device
+ *     (the current one).  `stream` must belong to that device.
+ *   - Every call on one device shares that device's array, and it keeps the
+ *     last call's contents (each launch clears its own counters first).  Calls
+ *     that overlap on one device race: calls on different streams, or from
+ *     different threads without ordering, corrupt each other's factors.
+ */
+int band_getrf_batched_noalloc(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
+                               int64_t strideAB, int32_t *d_ipiv, int64_t strideP,
+                               int32_t *d_info, int64_t batch, void *stream);
+
+/*
  * band_getrs -- solve A X = B with the factors from band_getrf (the "lu(A) \
  * B" of Listings 1 and 2; xGBTRS, no transpose).  dB is n x nrhs,
  * column-major, leading dimension ldb >= max(1, n), overwritten with X.

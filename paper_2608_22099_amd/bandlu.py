@@ -43,6 +43,7 @@ EXPORTS = {
     "dense_to_band_batched": [_vp, _i64, _i64, _i64, _i64, _i64, _vp, _i64, _i64, _i64, _vp],
     "band_getrf": [_i64, _i64, _i64, _vp, _i64, _vp, _vp, _vp],
     "band_getrf_batched": [_i64, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _vp, _i64, _vp],
+    "band_getrf_batched_noalloc": [_i64, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _vp, _i64, _vp],
     "band_getrs": [_i64, _i64, _i64, _i64, _vp, _i64, _vp, _vp, _i64, _vp],
     "band_getrs_batched": [_i64, _i64, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _vp, _i64, _i64,
                            _i64, _vp],
@@ -205,6 +206,20 @@ def band_getrf_batched(AB, kl, ku, ipiv=None, info=None, variant=None):
     else:
         _call("band_getrf_ex", n, kl, ku, _ptr(AB), ldab, sAB, _ptr(ipiv), sP, _ptr(info), batch,
               _variant_code(variant), _stream())
+    return ipiv, info
+
+
+def band_getrf_batched_noalloc(AB, kl, ku, ipiv, info):
+    """band_getrf_batched without any device allocation, for callers that
+    cannot allocate: the caller passes ipiv (batch, n) and info (batch,), and
+    the wide-band kernel's scratch is the library's fixed per-device array."""
+    _check(AB, torch.float64, "AB", 3)
+    batch, n = AB.shape[0], AB.shape[1]
+    ldab = max(_ld(AB), 1)
+    sAB = AB.stride(0) if batch > 1 else ldab * n
+    sP = ipiv.stride(0) if batch > 1 else n
+    _call("band_getrf_batched_noalloc", n, kl, ku, _ptr(AB), ldab, sAB, _ptr(ipiv), sP,
+          _ptr(info), batch, _stream())
     return ipiv, info
 
 

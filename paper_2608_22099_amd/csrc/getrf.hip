@@ -31,6 +31,7 @@
 // rounding.  band_getrf_ex runs a named variant.
 #include <cfloat>
 #include <climits>
+#include <mutex>
 
 #include "bufio.hpp"
 #include "getrf_diag.hpp"
@@ -93,9 +94,10 @@ int launch_getrf_mfma(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ld
                       int64_t batch, hipStream_t s);
 int launch_getrf_wide(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
                       int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info,
-                      int64_t batch, hipStream_t s, void *scratch, size_t scratch_bytes);
+                      int64_t batch, hipStream_t s, void *ws, size_t ws_bytes);
 bool getrf_wide_fits(int64_t n, int64_t kl, int64_t ku, int64_t batch);
 bool getrf_wide_one_launch(int64_t n, int64_t kl, int64_t ku, int64_t batch);
+size_t getrf_wide_scratch_bytes(int64_t n, int64_t kl, int64_t ku, int64_t batch);
 
 namespace {
 
@@ -257,9 +259,13 @@ bool variant_fits(int v, int64_t n, int64_t kl, int64_t ku, int64_t ldab, int64_
     }
 }
 
+// ws / ws_bytes: a caller's scratch buffer for the persistent wide-band
+// kernel, or null to let it take one from the stream-ordered allocator (the
+// other kernels need none)
 int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
                  int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info,
-                 int64_t batch, int variant, hipStream_t s) {
+                 int64_t batch, int variant, hipStream_t s, void *ws = nullptr,
+                 size_t ws_bytes = 0) {
     if (batch == 0) return BANDLU_OK;
     if (n == 0) {
         hipLaunchKernelGGL(zero_info_kernel, dim3((unsigned)((batch + 255) / 256)), dim3(256), 0,
@@ -383,7 +389,7 @@ int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
         return launch_getrf_mfma(n, kl, ku, dAB, ldab, strideAB, d_ipiv, strideP, d_info, batch, s);
     if (v == BANDLU_GETRF_WIDE)
         return launch_getrf_wide(n, kl, ku, dAB, ldab, strideAB, d_ipiv, strideP, d_info, batch, s,
-                                 nullptr, 0);
+                                 ws, ws_bytes);
     GenParams P;
     P.AB = dAB;
     P.ipiv = d_ipiv;
@@ -477,4 +483,85 @@ extern "C" int band_getrf_ex(int64_t n, int64_t kl, int64_t ku, double *dAB, int
     }
     return launch_getrf(n, kl, ku, dAB, ldab, strideAB, d_ipiv, strideP, d_info, batch, variant,
                         as_stream(stream));
+}
+
+// ------------------------------------------------- no-allocation entry --
+// The persistent wide-band kernel's hand-off ring (counters and published
+// panels) lives in a fixed device array instead of stream-ordered memory, so
+// that a caller that cannot allocate can factor any band the library would
+// factor with it, up to kNoAllocScratchBytes of ring per matrix.  Every
+// device the entry point runs on holds its own copy of the array until the
+// process ends; host code reaches it only through the address looked up once
+// per device (the array's name is a host-side stand-in, not a device address).
+namespace bandlu {
+namespace {
+constexpr size_t kNoAllocScratchBytes = size_t(16) << 20;
+constexpr int kNoAllocMaxDevices = 64;
+std::mutex g_noalloc_mu;
+void *g_noalloc_ptr[kNoAllocMaxDevices];
+}  // namespace
+}  // namespace bandlu
+
+static __device__ __align__(256) char scratch[bandlu::kNoAllocScratchBytes];
+
+// device address of `scratch` on the current device
+static int noalloc_scratch(void **out) {
+    int dev = -1;
+    if (hipError_t e = hipGetDevice(&dev); e != hipSuccess)
+        return hip_fail(e, "band_getrf_batched_noalloc (current device)");
+    if (dev < 0 || dev >= kNoAllocMaxDevices) {
+        set_error("band_getrf_batched_noalloc: device %d beyond the %d the library tracks", dev,
+                  kNoAllocMaxDevices);
+        return BANDLU_ERR_UNSUPPORTED;
+    }
+    std::lock_guard<std::mutex> lock(g_noalloc_mu);
+    if (g_noalloc_ptr[dev] == nullptr) {
+        void *p = nullptr;
+        if (hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)); e != hipSuccess)
+            return hip_fail(e, "band_getrf_batched_noalloc (scratch address)");
+        g_noalloc_ptr[dev] = p;
+    }
+    *out = g_noalloc_ptr[dev];
+    return BANDLU_OK;
+}
+
+extern "C" int band_getrf_batched_noalloc(int64_t n, int64_t kl, int64_t ku, double *dAB,
+                                          int64_t ldab, int64_t strideAB, int32_t *d_ipiv,
+                                          int64_t strideP, int32_t *d_info, int64_t batch,
+                                          void *stream) {
+    clear_error();
+    const int64_t bmax = n > 1 ? n - 1 : 0;
+    BANDLU_ARG(n >= 0, 1, "band_getrf_batched_noalloc: n < 0");
+    BANDLU_ARG(kl >= 0 && kl <= bmax, 2, "band_getrf_batched_noalloc: kl out of range");
+    BANDLU_ARG(ku >= 0 && ku <= bmax, 3, "band_getrf_batched_noalloc: ku out of range");
+    BANDLU_ARG(n == 0 || batch == 0 || dAB != nullptr, 4, "band_getrf_batched_noalloc: dAB is null");
+    BANDLU_ARG(ldab >= 2 * kl + ku + 1, 5, "band_getrf_batched_noalloc: ldab < 2kl+ku+1");
+    BANDLU_ARG(batch <= 1 || strideAB >= ldab * n, 6,
+               "band_getrf_batched_noalloc: strideAB < ldab*n");
+    BANDLU_ARG(n == 0 || batch == 0 || d_ipiv != nullptr, 7,
+               "band_getrf_batched_noalloc: d_ipiv is null");
+    BANDLU_ARG(batch <= 1 || strideP >= n, 8, "band_getrf_batched_noalloc: strideP < n");
+    BANDLU_ARG(batch == 0 || d_info != nullptr, 9, "band_getrf_batched_noalloc: d_info is null");
+    BANDLU_ARG(batch >= 0, 10, "band_getrf_batched_noalloc: batch < 0");
+    if (n > kMaxN || batch > INT_MAX) {
+        set_error("band_getrf_batched_noalloc: sizes too large");
+        return BANDLU_ERR_UNSUPPORTED;
+    }
+    // the kernel band_getrf_batched would take; only the persistent wide-band
+    // one needs scratch, and it gets the fixed array
+    void *ws = nullptr;
+    size_t ws_bytes = 0;
+    if (n > 0 && batch > 0 && select_variant(n, kl, ku, batch) == BANDLU_GETRF_WIDE) {
+        const size_t per = getrf_wide_scratch_bytes(n, kl, ku, 1);
+        if (per > kNoAllocScratchBytes) {
+            set_error("band_getrf_batched_noalloc: kl = %lld, ku = %lld needs %zu bytes of "
+                      "scratch per matrix, beyond the %zu this entry point holds per device",
+                      (long long)kl, (long long)ku, per, kNoAllocScratchBytes);
+            return BANDLU_ERR_UNSUPPORTED;
+        }
+        if (int rc = noalloc_scratch(&ws); rc != BANDLU_OK) return rc;
+        ws_bytes = kNoAllocScratchBytes;
+    }
+    return launch_getrf(n, kl, ku, dAB, ldab, strideAB, d_ipiv, strideP, d_info, batch, 0,
+                        as_stream(stream), ws, ws_bytes);
 }

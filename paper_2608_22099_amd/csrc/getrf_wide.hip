@@ -734,18 +734,23 @@ int launch_getrf_wide(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ld
         return BANDLU_ERR_UNSUPPORTED;
     }
     const WideGeom g = wide_geom(n, kl, ku);
-    const int64_t chunk = wide_chunk(n, kl, ku, batch);
+    int64_t chunk = wide_chunk(n, kl, ku, batch);
     const int64_t per = wide_matrix_bytes(n, kl, ku);
-    const size_t need = size_t(chunk * per);
     bool own_alloc = false;
     if (scratch == nullptr) {
-        if (hipError_t e = hipMallocAsync(&scratch, need, s); e != hipSuccess)
+        if (hipError_t e = hipMallocAsync(&scratch, size_t(chunk * per), s); e != hipSuccess)
             return hip_fail(e, "band_getrf (wide-band scratch)");
         own_alloc = true;
-    } else if (scratch_bytes < need) {
-        set_error("band_getrf: the wide-band variant needs %zu bytes of scratch, %zu given", need,
-                  scratch_bytes);
-        return BANDLU_ERR_UNSUPPORTED;
+    } else {
+        // a caller's buffer: as many matrices per launch as it holds (the
+        // launches of a batch run one after another on the stream and reuse it)
+        if (scratch_bytes < size_t(per)) {
+            set_error("band_getrf: the wide-band variant needs %lld bytes of scratch per matrix "
+                      "for kl = %lld, ku = %lld; %zu available",
+                      (long long)per, (long long)kl, (long long)ku, scratch_bytes);
+            return BANDLU_ERR_UNSUPPORTED;
+        }
+        chunk = std::min<int64_t>(chunk, int64_t(scratch_bytes / size_t(per)));
     }
     WideParams P;
     P.AB = dAB;

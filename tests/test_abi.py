@@ -30,6 +30,7 @@ def lib():
     L.dense_to_band.argtypes = [vp, i64, i64, i64, i64, vp, i64, vp]
     L.band_getrf.argtypes = [i64, i64, i64, vp, i64, vp, vp, vp]
     L.band_getrf_batched.argtypes = [i64, i64, i64, vp, i64, i64, vp, i64, vp, i64, vp]
+    L.band_getrf_batched_noalloc.argtypes = [i64, i64, i64, vp, i64, i64, vp, i64, vp, i64, vp]
     L.band_getrs.argtypes = [i64, i64, i64, i64, vp, i64, vp, vp, i64, vp]
     L.band_getrf_variant.argtypes = [i64, i64, i64, i64]
     L.band_getrf_ex.argtypes = [i64, i64, i64, vp, i64, i64, vp, i64, vp, i64, ctypes.c_int, vp]
@@ -42,7 +43,8 @@ def test_header_declares_the_path():
     names = declared_functions()
     for f in ["band_detect", "band_detect_batched", "dense_to_band", "dense_to_band_batched",
               "band_getrf", "band_getrf_batched", "band_getrs", "band_getrs_batched",
-              "band_status_string", "band_last_error", "band_getrf_variant", "band_getrf_ex"]:
+              "band_status_string", "band_last_error", "band_getrf_variant", "band_getrf_ex",
+              "band_getrf_batched_noalloc"]:
         assert f in names
 
 
@@ -68,6 +70,13 @@ def test_argument_validation(lib):
     assert lib.band_getrf(10, 2, 3, fake, 8, fake, None, None) == -7
     assert lib.band_getrf_batched(10, 2, 3, fake, 8, 79, fake, 10, fake, 2, None) == -6
     assert lib.band_getrf_batched(10, 2, 3, fake, 8, 80, fake, 9, fake, 2, None) == -8
+    # the no-allocation form validates its arguments the same way
+    nf = lib.band_getrf_batched_noalloc
+    assert nf(10, 2, 3, fake, 8, 79, fake, 10, fake, 2, None) == -6
+    assert nf(10, 2, 3, fake, 8, 80, fake, 9, fake, 2, None) == -8
+    assert nf(10, 2, 3, fake, 7, 80, fake, 10, fake, 2, None) == -5
+    assert nf(10, 2, 3, fake, 8, 80, fake, 10, None, 2, None) == -9
+    assert b"noalloc" in lib.band_last_error()
     assert lib.band_getrs(10, 2, 3, -1, fake, 8, fake, fake, 10, None) == -4
     assert lib.band_getrs(10, 2, 3, 1, fake, 8, fake, fake, 9, None) == -9
     # band_getrf_ex: argument 11 is the variant; a variant that cannot take the
