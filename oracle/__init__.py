@@ -62,6 +62,12 @@ def lib():
         L.oracle_gbtrs.argtypes = [_i64, _i64, _i64, _i64, _pd, _i64, _pi32, _pd, _i64]
         L.oracle_dense_gepp.argtypes = [_i64, _pd, _i64, _pi32, _pi32]
         L.oracle_band_backward_error.argtypes = [_i64, _i64, _i64, _pd, _pd, _i64, _pi32]
+        L.oracle_band_trsv.argtypes = [_i64, _i64, _i64, _i64, _pd, _i64, _pd, _i64, _pi32]
+        L.oracle_gbtrs_t.argtypes = [_i64, _i64, _i64, _i64, _pd, _i64, _pi32, _pd, _i64]
+        L.oracle_gbtrf_mn.argtypes = [_i64, _i64, _i64, _i64, _pd, _i64, _pi32, _pi32, _pi64]
+        L.oracle_pbtrf.argtypes = [_i64, _i64, _pd, _i64, _pi32]
+        L.oracle_pbtrs.argtypes = [_i64, _i64, _i64, _pd, _i64, _pd, _i64]
+        L.oracle_is_symmetric_band.argtypes = [_pd, _i64, _i64, _i64]
         L.oracle_band_backward_error.restype = ctypes.c_double
         for f in ("oracle_detect", "oracle_dense_to_band", "oracle_gbtrf",
                   "oracle_gbtrs", "oracle_dense_gepp"):
@@ -177,3 +183,113 @@ def op_counts(n, kl, ku):
             "speedup_ratio": F / (I + C + f) if (I + C + f) else float("inf"),
             "speedup_constraint": (I + C + f) < F,
             "slowdown_constraint": I <= F}
+
+
+def _rhs(B, fn):
+    if B.dtype != np.float64 or not B.flags.c_contiguous or B.ndim != 2:
+        raise ValueError(f"{fn}: B must be C-contiguous float64 (nrhs, ldb)")
+    return B.shape
+
+
+def band_trsv(AB, kl, ku, B):
+    """Listing 1's triangular / diagonal solve in place on B (nrhs, ldb) from
+    the xGBTRF-layout band AB (n, ldab) with kl = 0 or ku = 0; returns info
+    (1-based index of the first zero diagonal entry, or 0)."""
+    n, ldab = AB.shape
+    _check_cm(AB, n, "band_trsv")
+    nrhs, ldb = _rhs(B, "band_trsv")
+    info = ctypes.c_int32(0)
+    rc = lib().oracle_band_trsv(n, kl, ku, nrhs, _dptr(AB), ldab, _dptr(B), max(ldb, 1),
+                                ctypes.byref(info))
+    _status(rc, "band_trsv")
+    return int(info.value)
+
+
+def gbtrs_t(AB, kl, ku, ipiv, B):
+    """Solve A^T x = b in place with the band LU factors; B is (nrhs, ldb)."""
+    n, ldab = AB.shape
+    _check_cm(AB, n, "gbtrs_t")
+    nrhs, ldb = _rhs(B, "gbtrs_t")
+    ipiv = np.ascontiguousarray(ipiv, dtype=np.int32)
+    rc = lib().oracle_gbtrs_t(n, kl, ku, nrhs, _dptr(AB), ldab, ipiv.ctypes.data_as(_pi32),
+                              _dptr(B), max(ldb, 1))
+    _status(rc, "gbtrs_t")
+    return B
+
+
+def gbtrf_mn(AB, m, kl, ku):
+    """Band LU of an m x n band matrix in place on AB (shape (n, ldab));
+    returns (ipiv int32 1-based, length min(m, n), info, flops)."""
+    n, ldab = AB.shape
+    _check_cm(AB, n, "gbtrf_mn")
+    ipiv = np.zeros(max(min(m, n), 1), dtype=np.int32)[:min(m, n)]
+    info = ctypes.c_int32(0)
+    fl = ctypes.c_int64(0)
+    rc = lib().oracle_gbtrf_mn(m, n, kl, ku, _dptr(AB), ldab, ipiv.ctypes.data_as(_pi32),
+                               ctypes.byref(info), ctypes.byref(fl))
+    _status(rc, "gbtrf_mn")
+    return ipiv, int(info.value), int(fl.value)
+
+
+def dense_to_band_mn(T, m, kl, ku, ldab=None):
+    """Pack an m x n column-major matrix (T[j, i] = A[i, j], T of shape (n, >= m))
+    into the xGBTRF layout (plain slot loop; every slot outside the matrix or
+    the band is +0.0)."""
+    n = T.shape[0]
+    ldab = 2 * kl + ku + 1 if ldab is None else ldab
+    AB = np.zeros((n, ldab))
+    for j in range(n):
+        for i in range(max(0, j - ku), min(m - 1, j + kl) + 1):
+            AB[j, kl + ku + i - j] = T[j, i]
+    return AB
+
+
+def pbtrf(AB, kd):
+    """Band Cholesky in place on the lower band AB (shape (n, ldab), element
+    (i, j) at AB[j, i - j]); returns info."""
+    n, ldab = AB.shape
+    _check_cm(AB, n, "pbtrf")
+    info = ctypes.c_int32(0)
+    rc = lib().oracle_pbtrf(n, kd, _dptr(AB), ldab, ctypes.byref(info))
+    _status(rc, "pbtrf")
+    return int(info.value)
+
+
+def pbtrs(AB, kd, B):
+    """Solve with the band Cholesky factor in place on B (nrhs, ldb)."""
+    n, ldab = AB.shape
+    _check_cm(AB, n, "pbtrs")
+    nrhs, ldb = _rhs(B, "pbtrs")
+    rc = lib().oracle_pbtrs(n, kd, nrhs, _dptr(AB), ldab, _dptr(B), max(ldb, 1))
+    _status(rc, "pbtrs")
+    return B
+
+
+def is_symmetric_band(T, kd):
+    """1 if A(i, j) == A(j, i) for 0 < i - j <= kd (T[j, i] = A[i, j])."""
+    n, lda = T.shape
+    _check_cm(T, n, "is_symmetric_band")
+    return int(lib().oracle_is_symmetric_band(_dptr(T), n, max(lda, 1), kd))
+
+
+def lower_band(T, kd, ldab=None):
+    """The lower band of a symmetric matrix in LAPACK's lower layout, element
+    (i, j), j <= i <= j + kd, at AB[j, i - j]; other slots +0.0."""
+    n = T.shape[0]
+    ldab = kd + 1 if ldab is None else ldab
+    AB = np.zeros((n, ldab))
+    for j in range(n):
+        for i in range(j, min(n - 1, j + kd) + 1):
+            AB[j, i - j] = T[j, i]
+    return AB
+
+
+def detect_convert(T, kl_cap, ku_cap):
+    """The fused identify-and-convert pass as its definition: detection with
+    the caps, and when no cap is exceeded the band of the detected (kl, ku)
+    in the xGBTRF layout.  Returns (kl, ku, exceeded, AB or None)."""
+    kl, ku, ex, _ = detect(T, kl_cap, ku_cap)
+    if ex:
+        return kl, ku, ex, None
+    AB, _ = dense_to_band(T, kl, ku)
+    return kl, ku, ex, AB

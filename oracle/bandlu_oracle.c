@@ -349,3 +349,255 @@ double oracle_band_backward_error(int64_t n, int64_t kl, int64_t ku, const doubl
     if (den == 0.0L) return num == 0.0L ? 0.0 : INFINITY;
     return (double)(sqrtl(num) / (sqrtl(den) * (long double)n * (long double)DBL_EPSILON));
 }
+
+/* ---------------------------------------------------------------------------
+ * Listing 1's triangular and diagonal branches (Sec. I-C): when the detected
+ * band has ku = 0 (lower triangular), kl = 0 (upper triangular) or both
+ * (diagonal), A x = b is solved by substitution straight from the band array,
+ * with no factorisation.  AB is in the xGBTRF layout of the conversion step
+ * (element (i, j) at AB[kl + ku + i - j + j*ldab]), nrhs right-hand sides in
+ * column-major B, solved in place.
+ *
+ *   lower (ku = 0):  for j = 0..n-1:   b[j] = b[j] / A(j,j);
+ *                                      b[i] = fma(-A(i,j), b[j], b[i]), i = j+1..min(n-1, j+kl)
+ *   upper (kl = 0):  for j = n-1..0:   b[j] = b[j] / A(j,j);
+ *                                      b[i] = fma(-A(i,j), b[j], b[i]), i = max(0, j-ku)..j-1
+ *   (kl = ku = 0 is both: b[j] = b[j] / A(j,j).)
+ *
+ * *info = 0, or j+1 for the first exactly-zero diagonal entry A(j,j); the
+ * substitution runs regardless (a zero divisor gives IEEE infinities or NaN).
+ * Returns -3 if the band is not triangular (kl > 0 and ku > 0).
+ * ------------------------------------------------------------------------- */
+int oracle_band_trsv(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *AB,
+                     int64_t ldab, double *B, int64_t ldb, int32_t *info)
+{
+    if (n < 0) return -1;
+    if (kl < 0 || kl > imax(0, n - 1)) return -2;
+    if (ku < 0 || ku > imax(0, n - 1)) return -3;
+    if (kl > 0 && ku > 0) return -3;
+    if (nrhs < 0) return -4;
+    if (ldab < 2 * kl + ku + 1) return -6;
+    if (ldb < imax(1, n)) return -8;
+    const int64_t kv = kl + ku;
+#define AT(i, c) AB[kv + (i) - (c) + (c) * ldab]
+    *info = 0;
+    for (int64_t j = 0; j < n; ++j) {
+        if (AT(j, j) == 0.0) {
+            *info = (int32_t)(j + 1);
+            break;
+        }
+    }
+    for (int64_t k = 0; k < nrhs; ++k) {
+        double *b = B + k * ldb;
+        if (ku == 0) {
+            for (int64_t j = 0; j < n; ++j) {
+                b[j] = b[j] / AT(j, j);
+                for (int64_t i = j + 1; i <= imin(n - 1, j + kl); ++i)
+                    b[i] = fma(-AT(i, j), b[j], b[i]);
+            }
+        } else {
+            for (int64_t j = n - 1; j >= 0; --j) {
+                b[j] = b[j] / AT(j, j);
+                for (int64_t i = imax(0, j - ku); i < j; ++i) b[i] = fma(-AT(i, j), b[j], b[i]);
+            }
+        }
+    }
+#undef AT
+    return 0;
+}
+
+/* ---------------------------------------------------------------------------
+ * Solve with the transpose, A^T x = b, from the band LU factors (the general
+ * "A \ B" of Listing 1 applied to A^T; xGBTRS with trans = 'T').  With
+ * A = P_0 L_0 P_1 L_1 ... U (product form), A^T = U^T ... L_1^T P_1 L_0^T P_0:
+ *
+ *   U^T pass, forward:  for j = 0..n-1:
+ *       b[j] = fma(-U(i,j), b[i], b[j]) for i = max(0, j-kv)..j-1 (ascending);
+ *       b[j] = b[j] / U(j,j)
+ *   L^T pass, backward (kl > 0):  for j = n-2..0, km = min(kl, n-1-j):
+ *       b[j] = fma(-l_t, b[j+t], b[j]) for t = 1..km (ascending), l_t = AB row kv+t of column j;
+ *       swap b[j] and b[ipiv[j]-1]
+ * ------------------------------------------------------------------------- */
+int oracle_gbtrs_t(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *AB,
+                   int64_t ldab, const int32_t *ipiv, double *B, int64_t ldb)
+{
+    if (n < 0) return -1;
+    if (kl < 0 || kl > imax(0, n - 1)) return -2;
+    if (ku < 0 || ku > imax(0, n - 1)) return -3;
+    if (nrhs < 0) return -4;
+    if (ldab < 2 * kl + ku + 1) return -6;
+    if (ldb < imax(1, n)) return -9;
+    const int64_t kv = kl + ku;
+#define AT(i, c) AB[kv + (i) - (c) + (c) * ldab]
+    for (int64_t k = 0; k < nrhs; ++k) {
+        double *b = B + k * ldb;
+        for (int64_t j = 0; j < n; ++j) {
+            for (int64_t i = imax(0, j - kv); i < j; ++i) b[j] = fma(-AT(i, j), b[i], b[j]);
+            b[j] = b[j] / AT(j, j);
+        }
+        if (kl > 0) {
+            for (int64_t j = n - 2; j >= 0; --j) {
+                int64_t km = imin(kl, n - 1 - j);
+                for (int64_t t = 1; t <= km; ++t) b[j] = fma(-AT(j + t, j), b[j + t], b[j]);
+                int64_t l = ipiv[j] - 1;
+                if (l != j) {
+                    const double bl = b[l];
+                    b[l] = b[j];
+                    b[j] = bl;
+                }
+            }
+        }
+    }
+#undef AT
+    return 0;
+}
+
+/* ---------------------------------------------------------------------------
+ * Band LU with partial pivoting of a rectangular m x n band matrix (xGBTRF
+ * with m != n; the same column steps as oracle_gbtrf, Sec. III-A), for
+ * j = 0..min(m,n)-1 with km = min(kl, m-1-j) candidates below the diagonal
+ * and the update extent ju = max(ju, min(j + ku + p, n-1)).  Element (i, j),
+ * 0 <= i < m, lives at AB[kl + ku + i - j + j*ldab]; ipiv has min(m, n)
+ * entries.  Fill slots inside the matrix (AB rows 0..kl-1 whose matrix row
+ * is >= 0) start at zero.
+ * ------------------------------------------------------------------------- */
+int oracle_gbtrf_mn(int64_t m, int64_t n, int64_t kl, int64_t ku, double *AB, int64_t ldab,
+                    int32_t *ipiv, int32_t *info, int64_t *flops)
+{
+    if (m < 0) return -1;
+    if (n < 0) return -2;
+    if (kl < 0 || kl > imax(0, m - 1)) return -3;
+    if (ku < 0 || ku > imax(0, n - 1)) return -4;
+    if (ldab < 2 * kl + ku + 1) return -6;
+    const int64_t kv = kl + ku;
+    int64_t count = 0;
+    *info = 0;
+#define AT(i, c) AB[kv + (i) - (c) + (c) * ldab]
+    for (int64_t c = 0; c < n; ++c)
+        for (int64_t r = imax(0, kv - c); r < kl; ++r)
+            if (r - kv + c < m) AB[r + c * ldab] = 0.0;
+    int64_t ju = 0;
+    const int64_t steps = imin(m, n);
+    for (int64_t j = 0; j < steps; ++j) {
+        const int64_t km = imin(kl, m - 1 - j);
+        int64_t p = 0;
+        double best = fabs(AT(j, j));
+        for (int64_t t = 1; t <= km; ++t) {
+            const double v = fabs(AT(j + t, j));
+            if (v > best) {
+                best = v;
+                p = t;
+            }
+        }
+        ipiv[j] = (int32_t)(j + p + 1);
+        if (AT(j + p, j) == 0.0) {
+            if (*info == 0) *info = (int32_t)(j + 1);
+            continue;
+        }
+        ju = imax(ju, imin(n - 1, j + ku + p));
+        for (int64_t c = j; p != 0 && c <= ju; ++c) {
+            const double t0 = AT(j, c);
+            AT(j, c) = AT(j + p, c);
+            AT(j + p, c) = t0;
+        }
+        if (km == 0) continue;
+        const double piv = AT(j, j);
+        if (fabs(piv) >= DBL_MIN) {
+            const double r = 1.0 / piv;
+            for (int64_t t = 1; t <= km; ++t) AT(j + t, j) *= r;
+        } else {
+            for (int64_t t = 1; t <= km; ++t) AT(j + t, j) /= piv;
+        }
+        count += km;
+        for (int64_t c = j + 1; c <= ju; ++c)
+            for (int64_t t = 1; t <= km; ++t)
+                AT(j + t, c) = fma(-AT(j + t, j), AT(j, c), AT(j + t, c));
+        count += 2 * km * (ju - j);
+    }
+#undef AT
+    if (flops) *flops = count;
+    return 0;
+}
+
+/* ---------------------------------------------------------------------------
+ * Band Cholesky, A = L L^T, for a symmetric positive definite band matrix
+ * with kd sub-diagonals (the Cholesky case the paper names beside LU, end of
+ * Sec. II-B, on the symmetric structure of Sec. II-A; xPBTRF, lower).  The
+ * lower triangle is stored as in LAPACK: element (i, j), j <= i <= j+kd, at
+ * AB[i - j + j*ldab], ldab >= kd+1.  Right-looking, column by column:
+ *
+ *   for j = 0..n-1, kn = min(kd, n-1-j):
+ *     d = A(j,j); if not (d > 0): info = j+1, stop (A(j,j) keeps d)
+ *     d = sqrt(d); A(j,j) = d; r = 1/d; L(i,j) = A(i,j) * r, i = j+1..j+kn
+ *     A(i,c) = fma(-L(i,j), L(c,j), A(i,c)) for c = j+1..j+kn, i = c..j+kn
+ * ------------------------------------------------------------------------- */
+int oracle_pbtrf(int64_t n, int64_t kd, double *AB, int64_t ldab, int32_t *info)
+{
+    if (n < 0) return -1;
+    if (kd < 0 || kd > imax(0, n - 1)) return -2;
+    if (ldab < kd + 1) return -4;
+#define LT(i, c) AB[(i) - (c) + (c) * ldab]
+    *info = 0;
+    for (int64_t j = 0; j < n; ++j) {
+        const int64_t kn = imin(kd, n - 1 - j);
+        const double d0 = LT(j, j);
+        if (!(d0 > 0.0)) {
+            *info = (int32_t)(j + 1);
+            break;
+        }
+        const double d = sqrt(d0);
+        LT(j, j) = d;
+        const double r = 1.0 / d;
+        for (int64_t i = j + 1; i <= j + kn; ++i) LT(i, j) = LT(i, j) * r;
+        for (int64_t c = j + 1; c <= j + kn; ++c)
+            for (int64_t i = c; i <= j + kn; ++i) LT(i, c) = fma(-LT(i, j), LT(c, j), LT(i, c));
+    }
+#undef LT
+    return 0;
+}
+
+/* ---------------------------------------------------------------------------
+ * Solve A x = b with the band Cholesky factor (xPBTRS, lower):
+ *   L y = b,   forward:  for j = 0..n-1:  b[j] = b[j] / L(j,j);
+ *                                         b[i] = fma(-L(i,j), b[j], b[i]), i = j+1..min(n-1, j+kd)
+ *   L^T x = y, backward: for j = n-1..0:  b[j] = b[j] / L(j,j);
+ *                                         b[i] = fma(-L(j,i), b[j], b[i]), i = max(0, j-kd)..j-1
+ * ------------------------------------------------------------------------- */
+int oracle_pbtrs(int64_t n, int64_t kd, int64_t nrhs, const double *AB, int64_t ldab, double *B,
+                 int64_t ldb)
+{
+    if (n < 0) return -1;
+    if (kd < 0 || kd > imax(0, n - 1)) return -2;
+    if (nrhs < 0) return -3;
+    if (ldab < kd + 1) return -5;
+    if (ldb < imax(1, n)) return -7;
+#define LT(i, c) AB[(i) - (c) + (c) * ldab]
+    for (int64_t k = 0; k < nrhs; ++k) {
+        double *b = B + k * ldb;
+        for (int64_t j = 0; j < n; ++j) {
+            b[j] = b[j] / LT(j, j);
+            for (int64_t i = j + 1; i <= imin(n - 1, j + kd); ++i) b[i] = fma(-LT(i, j), b[j], b[i]);
+        }
+        for (int64_t j = n - 1; j >= 0; --j) {
+            b[j] = b[j] / LT(j, j);
+            for (int64_t i = imax(0, j - kd); i < j; ++i) b[i] = fma(-LT(j, i), b[j], b[i]);
+        }
+    }
+#undef LT
+    return 0;
+}
+
+/* ---------------------------------------------------------------------------
+ * Symmetry of a band (the symmetric structure of Sec. II-A's first step,
+ * examined as Listing 1's text describes): 1 if A(i,j) == A(j,i) under IEEE
+ * comparison for every 0 < i-j <= kd (so -0.0 matches +0.0 and a NaN matches
+ * nothing), else 0.  Entries beyond kd are not examined (the detected
+ * bandwidths already say they are zero).
+ * ------------------------------------------------------------------------- */
+int oracle_is_symmetric_band(const double *A, int64_t n, int64_t lda, int64_t kd)
+{
+    for (int64_t j = 0; j < n; ++j)
+        for (int64_t i = j + 1; i <= imin(n - 1, j + kd); ++i)
+            if (!(A[i + j * lda] == A[j + i * lda])) return 0;
+    return 1;
+}

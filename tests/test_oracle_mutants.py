@@ -32,6 +32,29 @@ MUTANTS = {
     "tiny_pivot_threshold": ("if (fabs(piv) >= DBL_MIN) {\n                    double r = 1.0 / piv;",
                              "if (fabs(piv) > 0.0) {\n                    double r = 1.0 / piv;"),
     "fill_zeroing": ("r < kl; ++r) AB[r + c * ldab] = 0.0;", "r < kl; ++r) (void)0;"),
+    # triangular / diagonal solve
+    "trsv_lower_range": ("for (int64_t i = j + 1; i <= imin(n - 1, j + kl); ++i)\n                    b[i]",
+                         "for (int64_t i = j + 1; i <= imin(n - 1, j + kl - 1); ++i)\n                    b[i]"),
+    "trsv_upper_no_divide": ("b[j] = b[j] / AT(j, j);\n                for (int64_t i = imax(0, j - ku); i < j; ++i)",
+                             "b[j] = b[j];\n                for (int64_t i = imax(0, j - ku); i < j; ++i)"),
+    "trsv_info_index": ("if (AT(j, j) == 0.0) {\n            *info = (int32_t)(j + 1);",
+                        "if (AT(j, j) == 0.0) {\n            *info = (int32_t)(j);"),
+    # transposed solve
+    "gbtrs_t_transposed_operand": ("b[j] = fma(-AT(i, j), b[i], b[j]);", "b[j] = fma(-AT(j, i), b[i], b[j]);"),
+    "gbtrs_t_lpass_index": ("b[j] = fma(-AT(j + t, j), b[j + t], b[j]);",
+                            "b[j] = fma(-AT(j + t, j), b[j + t - 1], b[j]);"),
+    "gbtrs_t_dropped_swap": ("b[l] = b[j];\n                    b[j] = bl;", "(void)bl;"),
+    # rectangular LU
+    "gbtrf_mn_candidates": ("const int64_t km = imin(kl, m - 1 - j);", "const int64_t km = imin(kl, n - 1 - j);"),
+    "gbtrf_mn_extent": ("ju = imax(ju, imin(n - 1, j + ku + p));", "ju = imax(ju, imin(n - 1, j + ku));"),
+    # band Cholesky
+    "pbtrf_update_operand": ("LT(i, c) = fma(-LT(i, j), LT(c, j), LT(i, c));",
+                             "LT(i, c) = fma(-LT(i, j), LT(i, j), LT(i, c));"),
+    "pbtrf_no_sqrt": ("const double d = sqrt(d0);", "const double d = d0;"),
+    "pbtrf_pd_test": ("if (!(d0 > 0.0)) {", "if (d0 < 0.0) {"),
+    "pbtrs_backward_transpose": ("b[i] = fma(-LT(j, i), b[j], b[i]);", "b[i] = fma(-LT(i, j), b[j], b[i]);"),
+    "symmetric_compare": ("if (!(A[i + j * lda] == A[j + i * lda])) return 0;",
+                          "if (!(A[i + j * lda] == A[i + j * lda])) return 0;"),
 }
 
 

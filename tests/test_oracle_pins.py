@@ -464,3 +464,330 @@ class TestCostModel:
         assert all(1.9 < g < 2.1 for g in growth), growth
         s = [(n * n + 2 * n ** 3 / 3) / (2 * n ** 3 / 3) for n in (1000, 8000)]
         assert s[1] < s[0] < 1.01
+
+
+# --------------------------------------------------------------------------
+# triangular / diagonal solve from the band (Listing 1's istril / istriu
+# branches, Sec. I-C)
+# --------------------------------------------------------------------------
+def tri_band(n, kl, ku, seed, diag_shift=4.0):
+    T = random_band(n, kl, ku, seed)
+    T[np.arange(n), np.arange(n)] += diag_shift * np.sign(T[np.arange(n), np.arange(n)] + 0.5)
+    return T
+
+
+def lapack_tb(AB, kl, ku):
+    """xGBTRF-layout band (AB[j, r]) -> the (ldab, n) array LAPACK's xTBTRS reads."""
+    if ku == 0:  # lower: A(i, j) at row i - j
+        return np.ascontiguousarray(AB[:, kl:2 * kl + 1].T)
+    return np.ascontiguousarray(AB[:, 0:ku + 1].T)  # upper, kl = 0: row ku + i - j
+
+
+class TestTriangularSolve:
+    def test_hand_examples(self):
+        L = np.array([[2.0, 0, 0], [1, 4, 0], [0, 3, 8]])
+        U = L.T.copy()
+        D = np.diag([2.0, 4.0, 8.0])
+        for A, kl, ku, b, x in [(L, 1, 0, [2.0, 5, 11], [1.0, 1, 1]),
+                                (U, 0, 1, [3.0, 7, 8], [1.0, 1, 1]),
+                                (D, 0, 0, [1.0, 1, 1], [0.5, 0.25, 0.125])]:
+            AB, _ = oracle.dense_to_band(np.ascontiguousarray(A.T), kl, ku)
+            B = np.array([b])
+            assert oracle.band_trsv(AB, kl, ku, B) == 0
+            assert np.array_equal(B[0], x)
+
+    @pytest.mark.parametrize("seed", range(6))
+    def test_exact_integer_solutions(self, seed):
+        """Integer band entries, diagonal +-1 or +-2 and integer x: every
+        intermediate is an integer, so substitution is exact."""
+        rng = np.random.default_rng(700 + seed)
+        n = int(rng.integers(5, 30))
+        k = int(rng.integers(1, 6))
+        for kl, ku in ((k, 0), (0, k)):
+            A = np.zeros((n, n))
+            for j in range(n):
+                for i in range(max(0, j - ku), min(n - 1, j + kl) + 1):
+                    A[i, j] = float(rng.integers(-3, 4))
+                A[j, j] = float(rng.choice([-2.0, -1.0, 1.0, 2.0]))
+            x = rng.integers(-4, 5, size=n).astype(float)
+            # make b = A x with every x_j even where A(j,j) = +-2 divides exactly
+            b = A @ x
+            AB, _ = oracle.dense_to_band(np.ascontiguousarray(A.T), kl, ku)
+            B = b[None, :].copy()
+            assert oracle.band_trsv(AB, kl, ku, B) == 0
+            assert np.array_equal(B[0], x), (kl, ku)
+
+    @pytest.mark.parametrize("seed", range(8))
+    def test_vs_lapack_dtbtrs(self, seed):
+        rng = np.random.default_rng(710 + seed)
+        n = int(rng.integers(1, 200))
+        k = int(rng.integers(0, min(n, 40)))
+        for kl, ku in ((k, 0), (0, k)):
+            T = tri_band(n, kl, ku, 720 + seed)
+            AB, _ = oracle.dense_to_band(T, kl, ku)
+            B = rng.standard_normal((2, n))
+            ref, info = lapack.dtbtrs(lapack_tb(AB, kl, ku), B.T.copy(),
+                                      uplo="L" if ku == 0 else "U")
+            assert info == 0
+            got = B.copy()
+            assert oracle.band_trsv(AB, kl, ku, got) == 0
+            assert np.allclose(got, ref.T, rtol=1e-12, atol=1e-13 * np.abs(ref).max()), (kl, ku)
+
+    def test_dense_solve_triangular(self):
+        import scipy.linalg as sl
+        n, kl = 150, 7
+        T = tri_band(n, kl, 0, 730)
+        AB, _ = oracle.dense_to_band(T, kl, 0)
+        b = np.random.default_rng(731).standard_normal(n)
+        B = b[None, :].copy()
+        oracle.band_trsv(AB, kl, 0, B)
+        ref = sl.solve_triangular(T.T, b, lower=True)
+        assert np.allclose(B[0], ref, rtol=1e-12, atol=1e-13)
+
+    def test_zero_diagonal_info_and_not_triangular(self):
+        T = tri_band(20, 3, 0, 740)
+        T[11, 11] = 0.0
+        T[15, 15] = 0.0
+        AB, _ = oracle.dense_to_band(T, 3, 0)
+        B = np.ones((1, 20))
+        assert oracle.band_trsv(AB, 3, 0, B) == 12
+        assert np.all(np.isfinite(B[0, :11])) and not np.all(np.isfinite(B[0, 11:]))
+        AB2, _ = oracle.dense_to_band(random_band(20, 2, 2, 741), 2, 2)
+        with pytest.raises(ValueError):
+            oracle.band_trsv(AB2, 2, 2, np.ones((1, 20)))
+
+
+# --------------------------------------------------------------------------
+# transposed solve with the band LU factors (the general A \ B of Listing 1
+# applied to A^T; xGBTRS trans = 'T')
+# --------------------------------------------------------------------------
+def exact_solve(A, b):
+    """Exact rational Gaussian elimination (brute force, any pivot order)."""
+    from fractions import Fraction
+    n = len(b)
+    M = [[Fraction(float(A[i, j])) for j in range(n)] + [Fraction(float(b[i]))] for i in range(n)]
+    for c in range(n):
+        p = next(r for r in range(c, n) if M[r][c] != 0)
+        M[c], M[p] = M[p], M[c]
+        for r in range(c + 1, n):
+            f = M[r][c] / M[c][c]
+            if f:
+                M[r] = [a - f * bb for a, bb in zip(M[r], M[c])]
+    x = [Fraction(0)] * n
+    for i in range(n - 1, -1, -1):
+        s = M[i][n] - sum(M[i][j] * x[j] for j in range(i + 1, n))
+        x[i] = s / M[i][i]
+    return np.array([float(v) for v in x])
+
+
+class TestTransposedSolve:
+    def test_hand_example(self):
+        A = np.array([[1.0, 2, 0], [5, 1, 3], [0, 4, 1]])
+        AB, _ = oracle.dense_to_band(np.ascontiguousarray(A.T), 1, 1)
+        ipiv, info, _ = oracle.gbtrf(AB, 1, 1)
+        B = np.array([[6.0, 7.0, 4.0]])  # A^T [1, 1, 1]
+        oracle.gbtrs_t(AB, 1, 1, ipiv, B)
+        assert np.allclose(B[0], [1.0, 1.0, 1.0], rtol=0, atol=4e-16)
+
+    @pytest.mark.parametrize("seed", range(6))
+    def test_exact_rational(self, seed):
+        rng = np.random.default_rng(750 + seed)
+        n = int(rng.integers(2, 12))
+        kl = int(rng.integers(0, n))
+        ku = int(rng.integers(0, n))
+        T = random_band(n, kl, ku, 760 + seed)
+        A = T.T.copy()
+        if abs(np.linalg.det(A)) < 1e-3:
+            A += 3.0 * np.eye(n)
+            T = np.ascontiguousarray(A.T)
+        b = rng.standard_normal(n)
+        ref = exact_solve(A.T, b)
+        AB, _ = oracle.dense_to_band(T, kl, ku)
+        ipiv, info, _ = oracle.gbtrf(AB, kl, ku)
+        assert info == 0
+        B = b[None, :].copy()
+        oracle.gbtrs_t(AB, kl, ku, ipiv, B)
+        assert np.allclose(B[0], ref, rtol=1e-11, atol=1e-11 * np.abs(ref).max())
+
+    @pytest.mark.parametrize("seed", range(8))
+    def test_vs_lapack_dgbtrs_trans(self, seed):
+        rng = np.random.default_rng(770 + seed)
+        n = int(rng.integers(1, 300))
+        kl = int(rng.integers(0, min(n, 30)))
+        ku = int(rng.integers(0, min(n, 30)))
+        T = random_band(n, kl, ku, 780 + seed)
+        T[np.arange(n), np.arange(n)] += 2.0
+        AB, _ = oracle.dense_to_band(T, kl, ku)
+        ipiv, info, _ = oracle.gbtrf(AB, kl, ku)
+        B = rng.standard_normal((3, n))
+        ref, inf2 = lapack.dgbtrs(np.ascontiguousarray(AB.T), kl, ku, B.T.copy(), ipiv - 1,
+                                  trans=1)
+        got = B.copy()
+        oracle.gbtrs_t(AB, kl, ku, ipiv, got)
+        assert np.allclose(got, ref.T, rtol=1e-11, atol=1e-11 * np.abs(ref).max())
+        # and the residual of A^T x = b
+        r = T @ got.T - B.T  # T = A^T as a numpy matrix
+        assert np.abs(r).max() <= 1e-10 * (np.abs(T).sum(1).max() * np.abs(got).max() + 1)
+
+
+# --------------------------------------------------------------------------
+# rectangular m x n band LU (xGBTRF with m != n)
+# --------------------------------------------------------------------------
+class TestRectangularLU:
+    @pytest.mark.parametrize("seed", range(5))
+    def test_square_is_gbtrf_bitwise(self, seed):
+        rng = np.random.default_rng(800 + seed)
+        n = int(rng.integers(1, 120))
+        kl = int(rng.integers(0, min(n, 20)))
+        ku = int(rng.integers(0, min(n, 20)))
+        AB, _ = oracle.dense_to_band(random_band(n, kl, ku, 810 + seed), kl, ku)
+        A2 = AB.copy()
+        p1, i1, f1 = oracle.gbtrf(AB, kl, ku)
+        p2, i2, f2 = oracle.gbtrf_mn(A2, n, kl, ku)
+        assert np.array_equal(p1, p2) and i1 == i2 and f1 == f2
+        assert np.array_equal(bits(AB), bits(A2))
+
+    def test_hand_3x2(self):
+        A = np.array([[1.0, 2.0], [4.0, 3.0], [2.0, 1.0]])  # m = 3, n = 2
+        AB = oracle.dense_to_band_mn(np.ascontiguousarray(A.T), 3, 2, 1)
+        ipiv, info, _ = oracle.gbtrf_mn(AB, 3, 2, 1)
+        assert list(ipiv) == [2, 2] and info == 0
+        kv = 3
+        assert AB[0, kv] == 4.0 and AB[1, kv - 1] == 3.0 and AB[1, kv] == 1.25
+        assert AB[0, kv + 1] == 0.25 and AB[0, kv + 2] == 0.5 and AB[1, kv + 1] == -0.5 * (1 / 1.25)
+
+    @pytest.mark.parametrize("seed", range(10))
+    def test_vs_lapack_dgbtrf(self, seed):
+        rng = np.random.default_rng(820 + seed)
+        m = int(rng.integers(1, 150))
+        n = int(rng.integers(1, 150))
+        kl = int(rng.integers(0, m))
+        ku = int(rng.integers(0, n))
+        kl, ku = min(kl, 25), min(ku, 25)
+        A = np.zeros((m, n))
+        for j in range(n):
+            for i in range(max(0, j - ku), min(m - 1, j + kl) + 1):
+                A[i, j] = rng.standard_normal()
+        if seed % 3 == 0 and min(m, n) > 2:
+            A[:, min(m, n) // 2] = 0.0  # a zero column: info
+        T = np.zeros((n, max(m, 1)))
+        T[:, :m] = A.T
+        AB = oracle.dense_to_band_mn(T, m, kl, ku)
+        lu, ipiv_l, info_l = lapack.dgbtrf(np.ascontiguousarray(AB.T), kl, ku, m=m, n=n)
+        ipiv, info, _ = oracle.gbtrf_mn(AB, m, kl, ku)
+        assert info == info_l
+        assert np.array_equal(ipiv, ipiv_l[:min(m, n)] + 1)
+        assert np.allclose(AB, lu.T, rtol=1e-12, atol=1e-12 * max(1.0, np.abs(lu).max()))
+
+
+# --------------------------------------------------------------------------
+# band Cholesky (the Cholesky case beside LU, Sec. II-B; symmetric structure,
+# Sec. II-A)
+# --------------------------------------------------------------------------
+def spd_band(n, kd, seed):
+    rng = np.random.default_rng(seed)
+    A = np.zeros((n, n))
+    for j in range(n):
+        for i in range(j + 1, min(n - 1, j + kd) + 1):
+            A[i, j] = A[j, i] = rng.standard_normal()
+    A[np.arange(n), np.arange(n)] = np.abs(A).sum(0) + 1.0
+    return A
+
+
+class TestBandCholesky:
+    def test_hand_2x2(self):
+        AB = oracle.lower_band(np.array([[4.0, 2.0], [2.0, 5.0]]), 1)
+        assert oracle.pbtrf(AB, 1) == 0
+        assert np.array_equal(AB, [[2.0, 1.0], [2.0, 0.0]])
+
+    def test_exact_integer_factor(self):
+        """A = L L^T with integer L whose diagonal is 1, 2 or 4: every step is
+        exact, so the factor comes back exactly."""
+        rng = np.random.default_rng(850)
+        for n, kd in ((12, 3), (30, 5), (7, 6)):
+            L = np.zeros((n, n))
+            for j in range(n):
+                L[j, j] = float(rng.choice([1.0, 2.0, 4.0]))
+                for i in range(j + 1, min(n - 1, j + kd) + 1):
+                    L[i, j] = float(rng.integers(-3, 4))
+            A = L @ L.T
+            AB = oracle.lower_band(A, kd)
+            assert oracle.pbtrf(AB, kd) == 0
+            assert np.array_equal(AB, oracle.lower_band(np.ascontiguousarray(L.T), kd))
+
+    def test_toeplitz_closed_form(self):
+        n = 400
+        A = 2.0 * np.eye(n) - np.eye(n, k=1) - np.eye(n, k=-1)
+        AB = oracle.lower_band(A, 1)
+        assert oracle.pbtrf(AB, 1) == 0
+        j = np.arange(n, dtype=float)
+        assert np.allclose(AB[:, 0], np.sqrt((j + 2) / (j + 1)), rtol=4e-15, atol=0)
+        assert np.allclose(AB[:-1, 1], -np.sqrt((j[:-1] + 1) / (j[:-1] + 2)), rtol=4e-15, atol=0)
+
+    @pytest.mark.parametrize("seed", range(6))
+    def test_vs_lapack_dpbtrf_and_numpy(self, seed):
+        rng = np.random.default_rng(860 + seed)
+        n = int(rng.integers(1, 250))
+        kd = int(rng.integers(0, min(n, 40)))
+        A = spd_band(n, kd, 870 + seed)
+        AB = oracle.lower_band(A, kd)
+        ref, info_l = lapack.dpbtrf(np.ascontiguousarray(AB.T), lower=1)
+        assert oracle.pbtrf(AB, kd) == 0 and info_l == 0
+        assert np.allclose(AB, ref.T, rtol=1e-13, atol=1e-14 * np.abs(ref).max())
+        Ld = np.linalg.cholesky(A)
+        assert np.allclose(AB, oracle.lower_band(np.ascontiguousarray(Ld.T), kd), rtol=1e-12,
+                           atol=1e-13 * np.abs(Ld).max())
+
+    def test_not_positive_definite(self):
+        AB = oracle.lower_band(np.array([[1.0, 2.0], [2.0, 1.0]]), 1)
+        assert oracle.pbtrf(AB, 1) == 2
+        assert oracle.pbtrf(np.zeros((5, 2)), 1) == 1
+        A = spd_band(30, 4, 880)
+        A[17, 17] = np.nan
+        assert oracle.pbtrf(oracle.lower_band(A, 4), 4) == 18
+        A = spd_band(30, 4, 881)
+        A[9, 9] = -1.0
+        ref, info_l = lapack.dpbtrf(np.ascontiguousarray(oracle.lower_band(A, 4).T), lower=1)
+        assert oracle.pbtrf(oracle.lower_band(A, 4), 4) == info_l == 10
+
+    @pytest.mark.parametrize("seed", range(5))
+    def test_solve_vs_lapack_dpbtrs(self, seed):
+        rng = np.random.default_rng(890 + seed)
+        n = int(rng.integers(1, 300))
+        kd = int(rng.integers(0, min(n, 30)))
+        A = spd_band(n, kd, 900 + seed)
+        AB = oracle.lower_band(A, kd)
+        oracle.pbtrf(AB, kd)
+        B = rng.standard_normal((2, n))
+        ref, info = lapack.dpbtrs(np.ascontiguousarray(AB.T), B.T.copy(), lower=1)
+        got = B.copy()
+        oracle.pbtrs(AB, kd, got)
+        assert np.allclose(got, ref.T, rtol=1e-12, atol=1e-12 * np.abs(ref).max())
+        r = A @ got.T - B.T
+        assert np.abs(r).max() <= 1e-11 * (np.abs(A).sum(1).max() * np.abs(got).max() + 1)
+
+
+class TestSymmetryAndFusedConvert:
+    def test_symmetric_band(self):
+        A = spd_band(40, 5, 910)
+        T = np.ascontiguousarray(A.T)
+        assert oracle.is_symmetric_band(T, 5) == 1
+        T2 = T.copy()
+        T2[3, 6] = np.nextafter(T2[3, 6], np.inf)  # A(6, 3) != A(3, 6) by one ulp
+        assert oracle.is_symmetric_band(T2, 5) == 0
+        T3 = T.copy()
+        T3[10, 12], T3[12, 10] = 0.0, -0.0
+        assert oracle.is_symmetric_band(T3, 5) == 1
+        T4 = T.copy()
+        T4[10, 12] = T4[12, 10] = np.nan
+        assert oracle.is_symmetric_band(T4, 5) == 0
+        T5 = T.copy()
+        T5[0, 20] = 1.0  # beyond kd: not examined
+        assert oracle.is_symmetric_band(T5, 5) == 1
+
+    def test_fused_definition(self):
+        T = random_band(50, 3, 7, 920)
+        kl, ku, ex, AB = oracle.detect_convert(T, 10, 10)
+        assert (kl, ku, ex) == (3, 7, 0)
+        assert np.array_equal(bits(AB), bits(oracle.dense_to_band(T, 3, 7)[0]))
+        assert oracle.detect_convert(T, 2, 10)[2:] == (1, None)
