@@ -20,9 +20,12 @@
  *     ldab >= 2*kl + ku + 1.  Band rows 0..kl-1 hold the fill-in that row
  *     interchanges create in U (U has kl+ku superdiagonals).
  *   - Pointers prefixed d are device pointers (HBM of the current device);
- *     all buffers are owned and allocated by the caller.  The library keeps
- *     no allocation between calls, frees nothing and holds no global state
- *     other than a thread-local text of the last error.
+ *     all buffers passed in are owned and allocated by the caller.  The
+ *     library frees none of them and keeps no allocation between calls.  Its
+ *     only global state is a thread-local text of the last error and the
+ *     fixed per-device array of band_getrf_batched_noalloc.  The one kernel
+ *     that needs scratch (band_getrf's persistent wide-band variant) takes it
+ *     stream-ordered on the call's stream and returns it the same way.
  *   - stream is a hipStream_t (NULL = the legacy default stream).  Every call
  *     only enqueues work on that stream and returns; results are valid after
  *     the stream is synchronised.  No entry point synchronises or copies to
@@ -264,6 +267,152 @@ int band_getrs_ex(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double 
                   int64_t ldab, int64_t strideAB, const int32_t *d_ipiv, int64_t strideP,
                   double *dB, int64_t ldb, int64_t strideB, int64_t batch, int variant,
                   void *stream);
+
+/* ----------------------------------------------------------------------
+ * Beyond the LU path: the other branches and structures the paper points to
+ * ---------------------------------------------------------------------- */
+
+/*
+ * band_detect_convert -- steps 1 and 2 in one read of the dense matrix
+ * (Sec. II-A costs I(N) and C(N); Listing 2's detection and conversion).
+ * Detection as band_detect with caps kl_cap, ku_cap (both >= 0 here, at most
+ * n-1), d_out = {kl, ku, exceeded} (device int64[3]).  While it scans, every
+ * element inside the caps' band (-ku_cap <= i-j <= kl_cap) is also stored in
+ * dAB, laid out for the caps (ldab >= 2*kl_cap + ku_cap + 1, element (i, j)
+ * at row kl_cap + ku_cap + i - j of column j).
+ *   - When exceeded = 0, the band of the detected (kl, ku) starts
+ *     s = kl_cap + ku_cap - kl - ku rows into dAB.  So dAB + s with the same
+ *     ldab holds exactly what dense_to_band(A, kl, ku) writes (rows
+ *     0..2kl+ku, bitwise, fill rows and slots outside the matrix +0.0),
+ *     ready for band_getrf(n, kl, ku, dAB + s, ldab, ...).  The host learns
+ *     s from the one copy of d_out it makes anyway.  The other rows of dAB
+ *     hold unspecified values.
+ *   - When exceeded = 1, dAB's contents are unspecified (the scan may have
+ *     stopped early); convert with dense_to_band after a full detection.
+ * Callers size the caps to the memory they can spare for the band: the
+ * array has ldab * n doubles whatever the matrix turns out to be.
+ */
+int band_detect_convert(const double *dA, int64_t n, int64_t lda, int64_t kl_cap,
+                        int64_t ku_cap, int64_t *d_out, double *dAB, int64_t ldab, void *stream);
+
+/*
+ * band_detect_convert_batched -- band_detect_convert over `batch` matrices
+ * (matrix b at dA + b*strideA, its band array at dAB + b*strideAB), with
+ * d_out[3*b..3*b+2] per matrix and d_max = {max kl, max ku, any exceeded}.
+ * When no cap is exceeded every band array holds, s = kl_cap + ku_cap -
+ * max kl - max ku rows in, the band of the batch maximum (kl, ku), as
+ * dense_to_band_batched(A, max kl, max ku) writes it.
+ */
+int band_detect_convert_batched(const double *dA, int64_t n, int64_t lda, int64_t strideA,
+                                int64_t batch, int64_t kl_cap, int64_t ku_cap, int64_t *d_out,
+                                int64_t *d_max, double *dAB, int64_t ldab, int64_t strideAB,
+                                void *stream);
+
+/*
+ * band_trsv -- Listing 1's triangular and diagonal branches (Sec. I-C):
+ * when detection finds ku = 0 (lower triangular), kl = 0 (upper triangular)
+ * or both (diagonal), A X = B is solved by substitution straight from the
+ * converted band, with no factorisation.  dAB is the xGBTRF-layout band of
+ * dense_to_band (ldab >= 2kl+ku+1, A(i, j) at row kl+ku+i-j); nrhs columns
+ * of B (ldb >= n) are overwritten with X.
+ *   lower: for j = 0..n-1:  x_j = b_j / A(j,j); b_i = fma(-A(i,j), x_j, b_i), i = j+1..j+kl
+ *   upper: for j = n-1..0:  x_j = b_j / A(j,j); b_i = fma(-A(i,j), x_j, b_i), i = j-ku..j-1
+ * so X is bitwise that of those loops.  *d_info (int32) = 0, or j+1 for the
+ * first exactly-zero diagonal entry; the substitution runs regardless (IEEE
+ * infinities or NaN follow).  kl > 0 and ku > 0 together return -3.
+ */
+int band_trsv(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *dAB, int64_t ldab,
+              double *dB, int64_t ldb, int32_t *d_info, void *stream);
+
+/* band_trsv over `batch` systems: band b at dAB + b*strideAB, right-hand
+ * sides at dB + b*strideB (strideB >= ldb*nrhs), info at d_info[b]. */
+int band_trsv_batched(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *dAB,
+                      int64_t ldab, int64_t strideAB, double *dB, int64_t ldb, int64_t strideB,
+                      int32_t *d_info, int64_t batch, void *stream);
+
+/*
+ * band_getrs_t -- solve A^T X = B with band_getrf's factors: the general
+ * "A \ B" of Listing 1 (Sec. I-C) on the transpose (xGBTRS, trans = 'T').
+ * Arguments as band_getrs.  With A = P_0 L_0 P_1 L_1 ... U:
+ *   U^T pass, j = 0..n-1:  b_j = fma(-U(i,j), b_i, b_j) for i = j-kv..j-1 ascending; b_j /= U(j,j)
+ *   L^T pass, j = n-2..0:  b_j = fma(-l_t, b_{j+t}, b_j) for t = 1..km ascending;
+ *                          swap b_j and b_{ipiv[j]-1}
+ * X is bitwise that of those loops.  kl is limited to 7999 (the L^T pass
+ * keeps a window of kl + 192 entries in 64 KiB of LDS); beyond that the call
+ * returns BANDLU_ERR_UNSUPPORTED.
+ */
+int band_getrs_t(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *dAB,
+                 int64_t ldab, const int32_t *d_ipiv, double *dB, int64_t ldb, void *stream);
+
+/* band_getrs_t over `batch` systems, strides as band_getrs_batched. */
+int band_getrs_t_batched(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *dAB,
+                         int64_t ldab, int64_t strideAB, const int32_t *d_ipiv, int64_t strideP,
+                         double *dB, int64_t ldb, int64_t strideB, int64_t batch, void *stream);
+
+/*
+ * band_getrf_mn -- band LU with partial pivoting of a rectangular m x n band
+ * matrix (xGBTRF with m != n; the column steps of Sec. III-A's banded LU).
+ * Element (i, j), 0 <= i < m, at dAB[kl+ku+i-j + j*ldab], ldab >= 2kl+ku+1,
+ * 0 <= kl <= max(0, m-1), 0 <= ku <= max(0, n-1).  Column j = 0..min(m,n)-1
+ * picks its pivot among rows j..min(m-1, j+kl).  ipiv has min(m, n)
+ * entries; info and the update extent are as in band_getrf, and the factors
+ * are bitwise those of the unblocked algorithm.  m = n gives band_getrf's
+ * result.  One workgroup per matrix.
+ */
+int band_getrf_mn(int64_t m, int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
+                  int32_t *d_ipiv, int32_t *d_info, void *stream);
+
+/* band_getrf_mn over `batch` matrices (strideAB >= ldab*n, strideP >=
+ * min(m, n), batch <= 65535). */
+int band_getrf_mn_batched(int64_t m, int64_t n, int64_t kl, int64_t ku, double *dAB,
+                          int64_t ldab, int64_t strideAB, int32_t *d_ipiv, int64_t strideP,
+                          int32_t *d_info, int64_t batch, void *stream);
+
+/*
+ * band_is_symmetric -- the symmetric structure among those the first step of
+ * Sec. II-A identifies: *d_flag (device int32) = 1 if A(i,j) == A(j,i) for
+ * every 0 < i-j <= kd (IEEE comparison: -0.0 matches +0.0, a NaN matches
+ * nothing), else 0.  Reads only the band of the dense column-major matrix
+ * (lda >= max(1, n), 0 <= kd <= max(0, n-1)).
+ */
+int band_is_symmetric(const double *dA, int64_t n, int64_t lda, int64_t kd, int32_t *d_flag,
+                      void *stream);
+
+/*
+ * band_pbtrf -- band Cholesky A = L L^T of a symmetric positive definite band
+ * matrix: the Cholesky case the paper names beside LU (end of Sec. II-B);
+ * xPBTRF, lower.  The lower triangle sits in LAPACK's layout, A(i, j),
+ * j <= i <= j+kd, at dAB[i - j + j*ldab], ldab >= kd+1.  dense_to_band(A,
+ * kd, 0) gives this layout kd rows into its array.  It is overwritten by L.
+ *   - Column j: d = A(j,j).  If not d > 0, then *d_info = j+1 and the
+ *     factorisation stops; column j and the kd columns after it keep their
+ *     updated values, as in the unblocked algorithm.
+ *   - Otherwise L(j,j) = sqrt(d), L(i,j) = A(i,j) * (1/L(j,j)), and the
+ *     trailing triangle is updated with one fma per entry and step.  L is
+ *     bitwise that of the unblocked loops.
+ *   - *d_info = 0 on success.
+ */
+int band_pbtrf(int64_t n, int64_t kd, double *dAB, int64_t ldab, int32_t *d_info, void *stream);
+
+/* band_pbtrf over `batch` matrices (band b at dAB + b*strideAB, info at
+ * d_info[b]). */
+int band_pbtrf_batched(int64_t n, int64_t kd, double *dAB, int64_t ldab, int64_t strideAB,
+                       int32_t *d_info, int64_t batch, void *stream);
+
+/*
+ * band_pbtrs -- solve A X = B with band_pbtrf's factor (xPBTRS, lower):
+ * L Y = B forward (divide by L(j,j), then update the kd rows below) and
+ * L^T X = Y backward (divide, then update the kd rows above with L(j, i)),
+ * one fma per entry and step, bitwise those loops.  nrhs columns of B
+ * (ldb >= n), in place.
+ */
+int band_pbtrs(int64_t n, int64_t kd, int64_t nrhs, const double *dAB, int64_t ldab, double *dB,
+               int64_t ldb, void *stream);
+
+/* band_pbtrs over `batch` systems (strides as band_getrs_batched). */
+int band_pbtrs_batched(int64_t n, int64_t kd, int64_t nrhs, const double *dAB, int64_t ldab,
+                       int64_t strideAB, double *dB, int64_t ldb, int64_t strideB, int64_t batch,
+                       void *stream);
 
 /* Text for a status code (static storage).  The codes follow the LAPACK
  * convention that the paper's callees (xGBTRF, xGETRF; Sec. III-A) use for

@@ -52,6 +52,22 @@ EXPORTS = {
     "band_getrs_variant": [_i64, _i64, _i64, _i64, _i64],
     "band_getrs_ex": [_i64, _i64, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _vp, _i64, _i64, _i64,
                       ctypes.c_int, _vp],
+    "band_detect_convert": [_vp, _i64, _i64, _i64, _i64, _vp, _vp, _i64, _vp],
+    "band_detect_convert_batched": [_vp, _i64, _i64, _i64, _i64, _i64, _i64, _vp, _vp, _vp, _i64,
+                                    _i64, _vp],
+    "band_trsv": [_i64, _i64, _i64, _i64, _vp, _i64, _vp, _i64, _vp, _vp],
+    "band_trsv_batched": [_i64, _i64, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _i64, _vp, _i64,
+                          _vp],
+    "band_getrs_t": [_i64, _i64, _i64, _i64, _vp, _i64, _vp, _vp, _i64, _vp],
+    "band_getrs_t_batched": [_i64, _i64, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _vp, _i64, _i64,
+                             _i64, _vp],
+    "band_getrf_mn": [_i64, _i64, _i64, _i64, _vp, _i64, _vp, _vp, _vp],
+    "band_getrf_mn_batched": [_i64, _i64, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _vp, _i64, _vp],
+    "band_is_symmetric": [_vp, _i64, _i64, _i64, _vp, _vp],
+    "band_pbtrf": [_i64, _i64, _vp, _i64, _vp, _vp],
+    "band_pbtrf_batched": [_i64, _i64, _vp, _i64, _i64, _vp, _i64, _vp],
+    "band_pbtrs": [_i64, _i64, _i64, _vp, _i64, _vp, _i64, _vp],
+    "band_pbtrs_batched": [_i64, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _i64, _i64, _vp],
     "band_status_string": [ctypes.c_int],
     "band_last_error": [],
 }
@@ -280,4 +296,191 @@ def band_getrs_batched(AB, kl, ku, ipiv, B, variant=None):
     else:
         _call("band_getrs_ex", n, kl, ku, nrhs, _ptr(AB), ldab, sAB, _ptr(ipiv), sP, _ptr(B), ldb,
               sB, batch, _getrs_code(variant), _stream())
+    return B
+
+
+# ------------------------------------------------- fused detect + convert --
+def band_detect_convert(A, kl_cap, ku_cap, AB=None, out=None):
+    """Detection with caps and, in the same read, the band of the caps.
+
+    Returns (out, AB): out = device int64 (kl, ku, exceeded); AB an (n, ldab)
+    band array with ldab = 2*kl_cap + ku_cap + 1.  When exceeded is 0 the band
+    of the detected (kl, ku) is ``band_view(AB, kl_cap, ku_cap, kl, ku)``."""
+    _check(A, torch.float64, "A", 2)
+    n = A.shape[0]
+    if out is None:
+        out = torch.empty(3, dtype=torch.int64, device=A.device)
+    if AB is None:
+        AB = torch.empty((n, 2 * kl_cap + ku_cap + 1), dtype=torch.float64, device=A.device)
+    _check(AB, torch.float64, "AB", 2)
+    _call("band_detect_convert", _ptr(A), n, max(_ld(A), n, 1), kl_cap, ku_cap, _ptr(out),
+          _ptr(AB), max(_ld(AB), 1), _stream())
+    return out, AB
+
+
+def band_detect_convert_batched(A, kl_cap, ku_cap, AB=None, out=None, dmax=None):
+    """Batched form; returns (out (batch, 3), dmax (3,), AB (batch, n, ldab))."""
+    _check(A, torch.float64, "A", 3)
+    batch, n = A.shape[0], A.shape[1]
+    if out is None:
+        out = torch.empty((batch, 3), dtype=torch.int64, device=A.device)
+    if dmax is None:
+        dmax = torch.empty(3, dtype=torch.int64, device=A.device)
+    if AB is None:
+        AB = torch.empty((batch, n, 2 * kl_cap + ku_cap + 1), dtype=torch.float64, device=A.device)
+    _check(AB, torch.float64, "AB", 3)
+    lda, ldab = max(_ld(A), n, 1), max(_ld(AB), 1)
+    sA = A.stride(0) if batch > 1 else lda * n
+    sAB = AB.stride(0) if batch > 1 else ldab * n
+    _call("band_detect_convert_batched", _ptr(A), n, lda, sA, batch, kl_cap, ku_cap, _ptr(out),
+          _ptr(dmax), _ptr(AB), ldab, sAB, _stream())
+    return out, dmax, AB
+
+
+def band_view(AB, kl_cap, ku_cap, kl, ku):
+    """The xGBTRF band of (kl, ku) inside an array laid out for the caps: the
+    same storage, starting kl_cap + ku_cap - kl - ku rows into each column
+    (rows 0..2kl+ku of the view are the band; ldab stays that of AB)."""
+    s = kl_cap + ku_cap - kl - ku
+    return AB[..., s:s + 2 * kl + ku + 1]
+
+
+# ------------------------------------------- triangular / diagonal solve --
+def band_trsv(AB, kl, ku, B, info=None):
+    """Listing 1's triangular / diagonal solve in place on B (nrhs, ldb) from
+    the converted band (kl = 0 or ku = 0); returns info (device int32)."""
+    _check(AB, torch.float64, "AB", 2)
+    _check(B, torch.float64, "B", 2)
+    n = AB.shape[0]
+    if info is None:
+        info = torch.empty(1, dtype=torch.int32, device=AB.device)
+    _call("band_trsv", n, kl, ku, B.shape[0], _ptr(AB), max(_ld(AB), 1), _ptr(B),
+          max(_ld(B), n, 1), _ptr(info), _stream())
+    return info
+
+
+def band_trsv_batched(AB, kl, ku, B, info=None):
+    _check(AB, torch.float64, "AB", 3)
+    _check(B, torch.float64, "B", 3)
+    batch, n = AB.shape[0], AB.shape[1]
+    nrhs = B.shape[1]
+    if info is None:
+        info = torch.empty(batch, dtype=torch.int32, device=AB.device)
+    ldab, ldb = max(_ld(AB), 1), max(_ld(B), n, 1)
+    sAB = AB.stride(0) if batch > 1 else ldab * n
+    sB = B.stride(0) if batch > 1 else ldb * nrhs
+    _call("band_trsv_batched", n, kl, ku, nrhs, _ptr(AB), ldab, sAB, _ptr(B), ldb, sB, _ptr(info),
+          batch, _stream())
+    return info
+
+
+# ---------------------------------------------------------- transposed solve --
+def band_getrs_t(AB, kl, ku, ipiv, B):
+    """Solve A^T X = B in place with band_getrf's factors; B is (nrhs, ldb)."""
+    _check(AB, torch.float64, "AB", 2)
+    _check(ipiv, torch.int32, "ipiv", 1)
+    _check(B, torch.float64, "B", 2)
+    n = AB.shape[0]
+    _call("band_getrs_t", n, kl, ku, B.shape[0], _ptr(AB), max(_ld(AB), 1), _ptr(ipiv), _ptr(B),
+          max(_ld(B), n, 1), _stream())
+    return B
+
+
+def band_getrs_t_batched(AB, kl, ku, ipiv, B):
+    _check(AB, torch.float64, "AB", 3)
+    _check(ipiv, torch.int32, "ipiv", 2)
+    _check(B, torch.float64, "B", 3)
+    batch, n = AB.shape[0], AB.shape[1]
+    nrhs = B.shape[1]
+    ldab, ldb = max(_ld(AB), 1), max(_ld(B), n, 1)
+    sAB = AB.stride(0) if batch > 1 else ldab * n
+    sP = ipiv.stride(0) if batch > 1 else n
+    sB = B.stride(0) if batch > 1 else ldb * nrhs
+    _call("band_getrs_t_batched", n, kl, ku, nrhs, _ptr(AB), ldab, sAB, _ptr(ipiv), sP, _ptr(B),
+          ldb, sB, batch, _stream())
+    return B
+
+
+# ----------------------------------------------------- rectangular band LU --
+def band_getrf_mn(AB, m, kl, ku, ipiv=None, info=None):
+    """LU of the m x n band matrix in AB (shape (n, ldab)); returns (ipiv, info)."""
+    _check(AB, torch.float64, "AB", 2)
+    n = AB.shape[0]
+    if ipiv is None:
+        ipiv = torch.empty(min(m, n), dtype=torch.int32, device=AB.device)
+    if info is None:
+        info = torch.empty(1, dtype=torch.int32, device=AB.device)
+    _call("band_getrf_mn", m, n, kl, ku, _ptr(AB), max(_ld(AB), 1), _ptr(ipiv), _ptr(info),
+          _stream())
+    return ipiv, info
+
+
+def band_getrf_mn_batched(AB, m, kl, ku, ipiv=None, info=None):
+    _check(AB, torch.float64, "AB", 3)
+    batch, n = AB.shape[0], AB.shape[1]
+    if ipiv is None:
+        ipiv = torch.empty((batch, min(m, n)), dtype=torch.int32, device=AB.device)
+    if info is None:
+        info = torch.empty(batch, dtype=torch.int32, device=AB.device)
+    ldab = max(_ld(AB), 1)
+    sAB = AB.stride(0) if batch > 1 else ldab * n
+    sP = ipiv.stride(0) if batch > 1 else min(m, n)
+    _call("band_getrf_mn_batched", m, n, kl, ku, _ptr(AB), ldab, sAB, _ptr(ipiv), sP, _ptr(info),
+          batch, _stream())
+    return ipiv, info
+
+
+# ---------------------------------------------------------- band Cholesky --
+def band_is_symmetric(A, kd, flag=None):
+    """Device int32: 1 if A(i, j) == A(j, i) for 0 < i - j <= kd."""
+    _check(A, torch.float64, "A", 2)
+    n = A.shape[0]
+    if flag is None:
+        flag = torch.empty(1, dtype=torch.int32, device=A.device)
+    _call("band_is_symmetric", _ptr(A), n, max(_ld(A), n, 1), kd, _ptr(flag), _stream())
+    return flag
+
+
+def band_pbtrf(AB, kd, info=None):
+    """Band Cholesky in place on the lower band AB (shape (n, ldab), element
+    (i, j) at AB[j, i - j]); returns info (device int32)."""
+    _check(AB, torch.float64, "AB", 2)
+    n = AB.shape[0]
+    if info is None:
+        info = torch.empty(1, dtype=torch.int32, device=AB.device)
+    _call("band_pbtrf", n, kd, _ptr(AB), max(_ld(AB), 1), _ptr(info), _stream())
+    return info
+
+
+def band_pbtrf_batched(AB, kd, info=None):
+    _check(AB, torch.float64, "AB", 3)
+    batch, n = AB.shape[0], AB.shape[1]
+    if info is None:
+        info = torch.empty(batch, dtype=torch.int32, device=AB.device)
+    ldab = max(_ld(AB), 1)
+    sAB = AB.stride(0) if batch > 1 else ldab * n
+    _call("band_pbtrf_batched", n, kd, _ptr(AB), ldab, sAB, _ptr(info), batch, _stream())
+    return info
+
+
+def band_pbtrs(AB, kd, B):
+    """Solve with band_pbtrf's factor in place on B (nrhs, ldb)."""
+    _check(AB, torch.float64, "AB", 2)
+    _check(B, torch.float64, "B", 2)
+    n = AB.shape[0]
+    _call("band_pbtrs", n, kd, B.shape[0], _ptr(AB), max(_ld(AB), 1), _ptr(B), max(_ld(B), n, 1),
+          _stream())
+    return B
+
+
+def band_pbtrs_batched(AB, kd, B):
+    _check(AB, torch.float64, "AB", 3)
+    _check(B, torch.float64, "B", 3)
+    batch, n = AB.shape[0], AB.shape[1]
+    nrhs = B.shape[1]
+    ldab, ldb = max(_ld(AB), 1), max(_ld(B), n, 1)
+    sAB = AB.stride(0) if batch > 1 else ldab * n
+    sB = B.stride(0) if batch > 1 else ldb * nrhs
+    _call("band_pbtrs_batched", n, kd, nrhs, _ptr(AB), ldab, sAB, _ptr(B), ldb, sB, batch,
+          _stream())
     return B

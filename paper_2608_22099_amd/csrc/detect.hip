@@ -22,6 +22,23 @@ constexpr int kThreads = 256;
 constexpr int kUnroll = 8;
 typedef double dbl2 __attribute__((ext_vector_type(2)));
 
+// Fused conversion: every element read that lies in the band of the caps,
+// -pku <= i - j <= pkl, is also stored at AB[pkl + pku + i - j + j*ldab].
+struct Pack {
+    double *AB;
+    int64_t ldab, strideAB;
+    int pkl, pku;
+};
+
+template <bool PACK>
+__device__ __forceinline__ void pack_store(const Pack &pk, int64_t b, int i, int c, double v) {
+    if constexpr (PACK) {
+        const int d = i - c;
+        if (d >= -pk.pku && d <= pk.pkl)
+            pk.AB[b * pk.strideAB + int64_t(pk.pkl + pk.pku + d) + int64_t(c) * pk.ldab] = v;
+    }
+}
+
 struct DetectParams {
     const double *A;
     int64_t n, lda, strideA;
@@ -30,6 +47,7 @@ struct DetectParams {
     int64_t kl_cap, ku_cap; // INT64_MAX when not capped
     unsigned long long *out;   // [3 * batch]
     unsigned long long *dmax;  // [3] or null
+    Pack pk;
 };
 
 __global__ void detect_init(unsigned long long *out, int64_t count, unsigned long long *dmax) {
@@ -93,7 +111,7 @@ __device__ inline void detect_flush(const DetectParams &P, int64_t b, int kl_l, 
     }
 }
 
-template <bool VEC, bool CAPS>
+template <bool VEC, bool CAPS, bool PACK>
 __global__ __launch_bounds__(kThreads) void detect_kernel(DetectParams P) {
     const int lane = threadIdx.x & 63;
     const int64_t wave = (int64_t(blockIdx.x) * kThreads + threadIdx.x) >> 6;
@@ -128,11 +146,16 @@ __global__ __launch_bounds__(kThreads) void detect_kernel(DetectParams P) {
                         int i0 = 2 * (base + u * 64 + lane);
                         if (v[u].x != 0.0) { last = i0; first = min(first, i0); }
                         if (v[u].y != 0.0) { last = i0 + 1; first = min(first, i0 + 1); }
+                        if (PACK && base + u * 64 + lane < n2) {
+                            pack_store<PACK>(P.pk, b, i0, int(j), v[u].x);
+                            pack_store<PACK>(P.pk, b, i0 + 1, int(j), v[u].y);
+                        }
                     }
                 }
                 if ((n & 1) && lane == 0) {
                     int i0 = int(n - 1);
                     if (col[i0] != 0.0) { last = i0; first = min(first, i0); }
+                    pack_store<PACK>(P.pk, b, i0, int(j), col[i0]);
                 }
             } else {
                 const int nn = int(n);
@@ -147,6 +170,7 @@ __global__ __launch_bounds__(kThreads) void detect_kernel(DetectParams P) {
                     for (int u = 0; u < kUnroll; ++u) {
                         int i0 = base + u * 64 + lane;
                         if (v[u] != 0.0) { last = i0; first = min(first, i0); }
+                        if (PACK && i0 < nn) pack_store<PACK>(P.pk, b, i0, int(j), v[u]);
                     }
                 }
             }
@@ -193,9 +217,10 @@ struct FlatParams {
     unsigned long long *dmax;  // [3] (batched) or null
     int64_t chunks_per_matrix; // batched: n*n / kFlatChunk
     int log2n;                 // batched: n = 2^log2n
+    Pack pk;
 };
 
-template <bool CAPS, bool BATCHED>
+template <bool CAPS, bool BATCHED, bool PACK>
 __global__ __launch_bounds__(kThreads) void detect_flat_kernel(FlatParams P) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -247,6 +272,10 @@ __global__ __launch_bounds__(kThreads) void detect_flat_kernel(FlatParams P) {
             const int d = i - c;
             if (v[u].x != 0.0) { kl_t = max(kl_t, d); ku_t = max(ku_t, -d); }
             if (v[u].y != 0.0) { kl_t = max(kl_t, d + 1); ku_t = max(ku_t, -d - 1); }
+            if (PACK && f0 + e < P.total) {
+                pack_store<PACK>(P.pk, mat, i, c, v[u].x);
+                pack_store<PACK>(P.pk, mat, i + 1, c, v[u].y);
+            }
         }
 #pragma unroll
         for (int u = 0; u < kFlatU; ++u) v[u] = vn[u];
@@ -281,9 +310,29 @@ __global__ __launch_bounds__(kThreads) void detect_flat_kernel(FlatParams P) {
     }
 }
 
+// After a fused pass: the band of the detected (kl, ku) (batched: the batch
+// maximum) starts pkl + pku - kl - ku rows into each matrix's band array.
+// Write +0.0 into that view's fill rows (0..kl-1) and into its slots outside
+// the matrix, as the conversion step does; nothing when a cap was exceeded.
+__global__ __launch_bounds__(256) void pack_fixup_kernel(Pack pk, int64_t n, int64_t batch,
+                                                         const unsigned long long *klku) {
+    if (klku[2] != 0ull) return;
+    const int64_t kl = int64_t(klku[0]), ku = int64_t(klku[1]);
+    const int64_t rows = 2 * kl + ku + 1;
+    const int64_t shift = pk.pkl + pk.pku - kl - ku;
+    const int64_t total = batch * n * rows;
+    for (int64_t g = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; g < total;
+         g += int64_t(gridDim.x) * blockDim.x) {
+        const int64_t r = g % rows, bc = g / rows;
+        const int64_t c = bc % n, b = bc / n;
+        const int64_t i = c + r - kl - ku;
+        if (r < kl || i < 0 || i >= n) pk.AB[b * pk.strideAB + shift + r + c * pk.ldab] = 0.0;
+    }
+}
+
 int launch_detect(const double *dA, int64_t n, int64_t lda, int64_t strideA, int64_t batch,
                   int64_t kl_cap, int64_t ku_cap, int64_t *d_out, int64_t *d_max,
-                  hipStream_t s) {
+                  hipStream_t s, const Pack *pack = nullptr) {
     const int64_t count = 3 * batch;
     {
         int blocks = (int)std::min<int64_t>((count + 255) / 256, 1024);
@@ -295,6 +344,8 @@ int launch_detect(const double *dA, int64_t n, int64_t lda, int64_t strideA, int
     }
     if (n == 0 || batch == 0) return BANDLU_OK;
     const bool caps = kl_cap >= 0 || ku_cap >= 0;
+    const bool pk = pack != nullptr;
+    const Pack pkv = pk ? *pack : Pack{};
     const bool aligned = reinterpret_cast<uintptr_t>(dA) % 16 == 0;
     int log2n = 0;
     while ((int64_t(1) << log2n) < n) ++log2n;
@@ -313,12 +364,16 @@ int launch_detect(const double *dA, int64_t n, int64_t lda, int64_t strideA, int
         F.dmax = reinterpret_cast<unsigned long long *>(d_max);
         F.chunks_per_matrix = (n * n) / kFlatChunk;
         F.log2n = log2n;
+        F.pk = pkv;
         const int64_t grid = std::min<int64_t>(F.nchunks, int64_t(device_cu_count()) * 8);
-        auto k = single_flat ? (caps ? detect_flat_kernel<true, false> : detect_flat_kernel<false, false>)
-                             : (caps ? detect_flat_kernel<true, true> : detect_flat_kernel<false, true>);
+        auto k = pk ? (single_flat ? detect_flat_kernel<true, false, true> : detect_flat_kernel<true, true, true>)
+                 : single_flat ? (caps ? detect_flat_kernel<true, false, false> : detect_flat_kernel<false, false, false>)
+                               : (caps ? detect_flat_kernel<true, true, false> : detect_flat_kernel<false, true, false>);
         hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(kThreads), 0, s, F);
         BANDLU_CHECK_LAUNCH("band_detect (flat)");
-        if (batch_flat) {
+        // the batch maximum (also for a batch of one that took the
+        // single-matrix kernel, which publishes to d_out only)
+        if (batch_flat || d_max != nullptr) {
             hipLaunchKernelGGL(detect_batch_max, dim3(1), dim3(kThreads), 0, s,
                                reinterpret_cast<const unsigned long long *>(d_out), batch,
                                reinterpret_cast<unsigned long long *>(d_max));
@@ -341,10 +396,12 @@ int launch_detect(const double *dA, int64_t n, int64_t lda, int64_t strideA, int
     P.ku_cap = ku_cap < 0 ? INT64_MAX : ku_cap;
     P.out = reinterpret_cast<unsigned long long *>(d_out);
     P.dmax = reinterpret_cast<unsigned long long *>(d_max);
+    P.pk = pkv;
     const bool vec = (reinterpret_cast<uintptr_t>(dA) % 16 == 0) && (lda % 2 == 0) &&
                      (batch == 1 || strideA % 2 == 0);
-    auto k = vec ? (caps ? detect_kernel<true, true> : detect_kernel<true, false>)
-                 : (caps ? detect_kernel<false, true> : detect_kernel<false, false>);
+    auto k = pk ? (vec ? detect_kernel<true, true, true> : detect_kernel<false, true, true>)
+           : vec ? (caps ? detect_kernel<true, true, false> : detect_kernel<true, false, false>)
+                 : (caps ? detect_kernel<false, true, false> : detect_kernel<false, false, false>);
     hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(kThreads), 0, s, P);
     BANDLU_CHECK_LAUNCH("band_detect");
     return BANDLU_OK;
@@ -387,4 +444,84 @@ extern "C" int band_detect_batched(const double *dA, int64_t n, int64_t lda, int
     }
     return launch_detect(dA, n, lda, strideA, batch, kl_cap, ku_cap, d_out, d_max,
                          as_stream(stream));
+}
+
+// ------------------------------------------------ fused detect + convert --
+// Steps 1 and 2 in one read of the dense matrix (Sec. II-A: I(N) and C(N);
+// Listing 2's detection and conversion): detection under the caps, and every
+// element inside the caps' band stored into a band array laid out for the
+// caps; then the fix-up above.
+namespace bandlu {
+namespace {
+int detect_convert(const double *dA, int64_t n, int64_t lda, int64_t strideA, int64_t batch,
+                   int64_t kl_cap, int64_t ku_cap, int64_t *d_out, int64_t *d_max, double *dAB,
+                   int64_t ldab, int64_t strideAB, hipStream_t s) {
+    Pack pk;
+    pk.AB = dAB;
+    pk.ldab = ldab;
+    pk.strideAB = strideAB;
+    pk.pkl = (int)kl_cap;
+    pk.pku = (int)ku_cap;
+    if (int rc = launch_detect(dA, n, lda, strideA, batch, kl_cap, ku_cap, d_out, d_max, s, &pk);
+        rc != BANDLU_OK)
+        return rc;
+    if (n == 0 || batch == 0) return BANDLU_OK;
+    const int64_t total = batch * n * (2 * kl_cap + ku_cap + 1);
+    const unsigned grid = (unsigned)std::min<int64_t>((total + 255) / 256, int64_t(device_cu_count()) * 16);
+    hipLaunchKernelGGL(pack_fixup_kernel, dim3(grid), dim3(256), 0, s, pk, n, batch,
+                       reinterpret_cast<const unsigned long long *>(batch == 1 && d_max == nullptr ? d_out : d_max));
+    BANDLU_CHECK_LAUNCH("band_detect_convert (fix-up)");
+    return BANDLU_OK;
+}
+}  // namespace
+}  // namespace bandlu
+
+extern "C" int band_detect_convert(const double *dA, int64_t n, int64_t lda, int64_t kl_cap,
+                                   int64_t ku_cap, int64_t *d_out, double *dAB, int64_t ldab,
+                                   void *stream) {
+    clear_error();
+    const int64_t bmax = n > 1 ? n - 1 : 0;
+    BANDLU_ARG(n >= 0, 2, "band_detect_convert: n = %lld < 0", (long long)n);
+    BANDLU_ARG(lda >= (n > 1 ? n : 1), 3, "band_detect_convert: lda < max(1, n)");
+    BANDLU_ARG(kl_cap >= 0 && kl_cap <= bmax, 4, "band_detect_convert: kl_cap out of [0, max(0, n-1)]");
+    BANDLU_ARG(ku_cap >= 0 && ku_cap <= bmax, 5, "band_detect_convert: ku_cap out of [0, max(0, n-1)]");
+    BANDLU_ARG(d_out != nullptr, 6, "band_detect_convert: d_out is null");
+    BANDLU_ARG(n == 0 || dAB != nullptr, 7, "band_detect_convert: dAB is null");
+    BANDLU_ARG(ldab >= 2 * kl_cap + ku_cap + 1, 8, "band_detect_convert: ldab < 2kl_cap+ku_cap+1");
+    BANDLU_ARG(n == 0 || dA != nullptr, 1, "band_detect_convert: dA is null");
+    if (n > kMaxN || n * ldab > (int64_t(1) << 40)) {
+        set_error("band_detect_convert: sizes too large");
+        return BANDLU_ERR_UNSUPPORTED;
+    }
+    return detect_convert(dA, n, lda, lda * n, 1, kl_cap, ku_cap, d_out, nullptr, dAB, ldab,
+                          ldab * n, as_stream(stream));
+}
+
+extern "C" int band_detect_convert_batched(const double *dA, int64_t n, int64_t lda,
+                                           int64_t strideA, int64_t batch, int64_t kl_cap,
+                                           int64_t ku_cap, int64_t *d_out, int64_t *d_max,
+                                           double *dAB, int64_t ldab, int64_t strideAB,
+                                           void *stream) {
+    clear_error();
+    const int64_t bmax = n > 1 ? n - 1 : 0;
+    BANDLU_ARG(n >= 0, 2, "band_detect_convert_batched: n < 0");
+    BANDLU_ARG(lda >= (n > 1 ? n : 1), 3, "band_detect_convert_batched: lda < max(1, n)");
+    BANDLU_ARG(batch <= 1 || strideA >= lda * n, 4, "band_detect_convert_batched: strideA < lda*n");
+    BANDLU_ARG(batch >= 0, 5, "band_detect_convert_batched: batch < 0");
+    BANDLU_ARG(kl_cap >= 0 && kl_cap <= bmax, 6, "band_detect_convert_batched: kl_cap out of range");
+    BANDLU_ARG(ku_cap >= 0 && ku_cap <= bmax, 7, "band_detect_convert_batched: ku_cap out of range");
+    BANDLU_ARG(batch == 0 || d_out != nullptr, 8, "band_detect_convert_batched: d_out is null");
+    BANDLU_ARG(d_max != nullptr, 9, "band_detect_convert_batched: d_max is null");
+    BANDLU_ARG(n == 0 || batch == 0 || dAB != nullptr, 10, "band_detect_convert_batched: dAB is null");
+    BANDLU_ARG(ldab >= 2 * kl_cap + ku_cap + 1, 11,
+               "band_detect_convert_batched: ldab < 2kl_cap+ku_cap+1");
+    BANDLU_ARG(batch <= 1 || strideAB >= ldab * n, 12,
+               "band_detect_convert_batched: strideAB < ldab*n");
+    BANDLU_ARG(n == 0 || batch == 0 || dA != nullptr, 1, "band_detect_convert_batched: dA is null");
+    if (n > kMaxN || (n > 0 && batch > INT64_MAX / n)) {
+        set_error("band_detect_convert_batched: sizes too large");
+        return BANDLU_ERR_UNSUPPORTED;
+    }
+    return detect_convert(dA, n, lda, strideA, batch, kl_cap, ku_cap, d_out, d_max, dAB, ldab,
+                          strideAB, as_stream(stream));
 }

@@ -29,6 +29,7 @@
 // The window, blocked and generic kernels produce bitwise the factors of the
 // unblocked algorithm on finite data; the matrix-core variant agrees to
 // rounding.  band_getrf_ex runs a named variant.
+#include <algorithm>
 #include <cfloat>
 #include <climits>
 #include <mutex>
@@ -108,6 +109,7 @@ struct GenParams {
     int32_t *ipiv;
     int32_t *info;
     int64_t n, kl, ku, ldab, strideAB, strideP;
+    int64_t m;  // rows (m x n band matrix; m = n for the square factorisation)
 };
 
 // pivot key: |x|, with a NaN ranked first in position 0 and last elsewhere, so
@@ -125,7 +127,7 @@ __global__ __launch_bounds__(kGenThreads) void getrf_generic_kernel(GenParams P)
     const int64_t b = blockIdx.x;
     double *__restrict__ AB = P.AB + b * P.strideAB;
     int32_t *__restrict__ ipiv = P.ipiv + b * P.strideP;
-    const int64_t n = P.n, kl = P.kl, ku = P.ku, kv = kl + ku, ldab = P.ldab;
+    const int64_t n = P.n, m = P.m, kl = P.kl, ku = P.ku, kv = kl + ku, ldab = P.ldab;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     __shared__ double s_key[kGenThreads / 64];
     __shared__ int64_t s_idx[kGenThreads / 64];
@@ -136,15 +138,16 @@ __global__ __launch_bounds__(kGenThreads) void getrf_generic_kernel(GenParams P)
     if (kl > 0) {
         for (int64_t idx = tid; idx < n * kl; idx += kGenThreads) {
             const int64_t c = idx / kl, r = idx - c * kl;
-            if (r >= kv - c) AB[c * ldab + r] = 0.0;
+            if (r >= kv - c && r - kv + c < m) AB[c * ldab + r] = 0.0;
         }
     }
     __syncthreads();
 
     int64_t ju = 0;
     int32_t info = 0;
-    for (int64_t j = 0; j < n; ++j) {
-        const int64_t km = min(kl, n - 1 - j);
+    const int64_t steps = min(m, n);
+    for (int64_t j = 0; j < steps; ++j) {
+        const int64_t km = min(kl, m - 1 - j);
         double *colj = AB + j * ldab + kv;  // colj[t] = a(j+t, j)
         double bk = -2.0;
         int64_t bi = INT64_MAX;
@@ -395,6 +398,7 @@ int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
     P.ipiv = d_ipiv;
     P.info = d_info;
     P.n = n;
+    P.m = n;
     P.kl = kl;
     P.ku = ku;
     P.ldab = ldab;
@@ -564,4 +568,77 @@ extern "C" int band_getrf_batched_noalloc(int64_t n, int64_t kl, int64_t ku, dou
     }
     return launch_getrf(n, kl, ku, dAB, ldab, strideAB, d_ipiv, strideP, d_info, batch, 0,
                         as_stream(stream), ws, ws_bytes);
+}
+
+// ------------------------------------------------- rectangular m x n --
+// The band LU of an m x n band matrix (xGBTRF with m != n): the one-workgroup
+// kernel above with m rows, min(m, n) column steps and km = min(kl, m-1-j)
+// candidates per step; element (i, j), 0 <= i < m, at AB[kl+ku+i-j + j*ldab].
+namespace bandlu {
+namespace {
+int getrf_mn(int64_t m, int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
+             int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info, int64_t batch,
+             hipStream_t s) {
+    if (batch == 0) return BANDLU_OK;
+    GenParams P;
+    P.AB = dAB;
+    P.ipiv = d_ipiv;
+    P.info = d_info;
+    P.n = n;
+    P.m = m;
+    P.kl = kl;
+    P.ku = ku;
+    P.ldab = ldab;
+    P.strideAB = strideAB;
+    P.strideP = strideP;
+    hipLaunchKernelGGL(getrf_generic_kernel, dim3((unsigned)batch), dim3(kGenThreads), 0, s, P);
+    BANDLU_CHECK_LAUNCH("band_getrf_mn");
+    return BANDLU_OK;
+}
+}  // namespace
+}  // namespace bandlu
+
+extern "C" int band_getrf_mn(int64_t m, int64_t n, int64_t kl, int64_t ku, double *dAB,
+                             int64_t ldab, int32_t *d_ipiv, int32_t *d_info, void *stream) {
+    clear_error();
+    BANDLU_ARG(m >= 0, 1, "band_getrf_mn: m < 0");
+    BANDLU_ARG(n >= 0, 2, "band_getrf_mn: n < 0");
+    BANDLU_ARG(kl >= 0 && kl <= (m > 1 ? m - 1 : 0), 3, "band_getrf_mn: kl out of [0, max(0, m-1)]");
+    BANDLU_ARG(ku >= 0 && ku <= (n > 1 ? n - 1 : 0), 4, "band_getrf_mn: ku out of [0, max(0, n-1)]");
+    BANDLU_ARG(n == 0 || dAB != nullptr, 5, "band_getrf_mn: dAB is null");
+    BANDLU_ARG(ldab >= 2 * kl + ku + 1, 6, "band_getrf_mn: ldab < 2kl+ku+1");
+    BANDLU_ARG(m == 0 || n == 0 || d_ipiv != nullptr, 7, "band_getrf_mn: d_ipiv is null");
+    BANDLU_ARG(d_info != nullptr, 8, "band_getrf_mn: d_info is null");
+    if (m > kMaxN || n > kMaxN) {
+        set_error("band_getrf_mn: sizes >= 2^31 are not supported");
+        return BANDLU_ERR_UNSUPPORTED;
+    }
+    return getrf_mn(m, n, kl, ku, dAB, ldab, ldab * n, d_ipiv, std::min(m, n), d_info, 1,
+                    as_stream(stream));
+}
+
+extern "C" int band_getrf_mn_batched(int64_t m, int64_t n, int64_t kl, int64_t ku, double *dAB,
+                                     int64_t ldab, int64_t strideAB, int32_t *d_ipiv,
+                                     int64_t strideP, int32_t *d_info, int64_t batch,
+                                     void *stream) {
+    clear_error();
+    BANDLU_ARG(m >= 0, 1, "band_getrf_mn_batched: m < 0");
+    BANDLU_ARG(n >= 0, 2, "band_getrf_mn_batched: n < 0");
+    BANDLU_ARG(kl >= 0 && kl <= (m > 1 ? m - 1 : 0), 3, "band_getrf_mn_batched: kl out of range");
+    BANDLU_ARG(ku >= 0 && ku <= (n > 1 ? n - 1 : 0), 4, "band_getrf_mn_batched: ku out of range");
+    BANDLU_ARG(n == 0 || batch == 0 || dAB != nullptr, 5, "band_getrf_mn_batched: dAB is null");
+    BANDLU_ARG(ldab >= 2 * kl + ku + 1, 6, "band_getrf_mn_batched: ldab < 2kl+ku+1");
+    BANDLU_ARG(batch <= 1 || strideAB >= ldab * n, 7, "band_getrf_mn_batched: strideAB < ldab*n");
+    BANDLU_ARG(m == 0 || n == 0 || batch == 0 || d_ipiv != nullptr, 8,
+               "band_getrf_mn_batched: d_ipiv is null");
+    BANDLU_ARG(batch <= 1 || strideP >= std::min(m, n), 9,
+               "band_getrf_mn_batched: strideP < min(m, n)");
+    BANDLU_ARG(batch == 0 || d_info != nullptr, 10, "band_getrf_mn_batched: d_info is null");
+    BANDLU_ARG(batch >= 0, 11, "band_getrf_mn_batched: batch < 0");
+    if (m > kMaxN || n > kMaxN || batch > 65535) {
+        set_error("band_getrf_mn_batched: sizes too large");
+        return BANDLU_ERR_UNSUPPORTED;
+    }
+    return getrf_mn(m, n, kl, ku, dAB, ldab, strideAB, d_ipiv, strideP, d_info, batch,
+                    as_stream(stream));
 }

@@ -35,18 +35,23 @@ int launch_getrs_ring(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const dou
     P.strideB = strideB;
     P.n = (int)n;
     P.kl = (int)kl;
-    P.kv = (int)(kl + ku);
     P.nrhs = (int)nrhs;
     const int64_t systems = batch * nrhs;
     if (kl > 0 && n > 1) {
-        const int q = int(kl >> 6);
-        const RingLaunch f = q < 8 ? ring_launcher_fwd_0_7(q) : ring_launcher_fwd_8_15(q);
-        f(P, systems, s);
+        // unit L with the interchanges: column j's entries from the diagonal row kv
+        P.cb0 = kl + ku;
+        P.es = 1;
+        P.K = (int)kl;
+        P.nsteps = (int)n - 1;
+        ring_pass(kRingFwdLU, P.K)(P, systems, s);
         BANDLU_CHECK_LAUNCH("band_getrs (ring, forward)");
     }
-    const int q = int((kl + ku) >> 6);
-    const RingLaunch f = q < 8 ? ring_launcher_bwd_0_7(q) : ring_launcher_bwd_8_15(q);
-    f(P, systems, s);
+    // U: column n-1-j's entries from row 0 (U(col-kv+e, col))
+    P.cb0 = 0;
+    P.es = 1;
+    P.K = (int)(kl + ku);
+    P.nsteps = (int)n;
+    ring_pass(kRingBwd, P.K)(P, systems, s);
     BANDLU_CHECK_LAUNCH("band_getrs (ring, backward)");
     return BANDLU_OK;
 }

@@ -1,14 +1,21 @@
-// Solve with the band factors (xGBTRS, no transpose) for any band up to
-// kl + ku = 1023: the "lu(A) \ B" that Listings 1 and 2 end with.
+// Chains of column steps on one vector, for bands up to K = 1023: the passes
+// of the band solve with the LU factors (xGBTRS: the "lu(A) \ B" that
+// Listings 1 and 2 end with) and of the other substitutions built on them
+// (Listing 1's triangular solves, the transposed solve, the Cholesky solve).
 //
-// One workgroup of four wavefronts per right-hand side, one launch per pass
-// (forward: the row interchanges and unit L; backward: U with kl+ku
-// superdiagonals).  Both passes are the same chain of column steps; the
-// backward pass runs over reversed row positions (position q is row n-1-q),
-// so that in either pass step j finishes position j and updates positions
-// j+1..j+K (K = kl forward, kl+ku backward) with one fused multiply-add each,
-// in the order of the unblocked algorithm: the result is bitwise that of the
-// reference loops.
+// One workgroup of four wavefronts per right-hand side, one launch per pass.
+// Step j finishes position j and updates positions j+1..j+K with one fused
+// multiply-add each, in the order of the unblocked algorithm, so the result is
+// bitwise that of the reference loops.  The entries of step j are
+// AB[cb0 + col*ldab + e*es], e = 0..K, with col = j (forward) or n-1-j
+// (backward), so a step can read a column of the band (es = 1) or a row
+// (es = ldab-1).  Three modes:
+//   kRingFwdLU  forward, unit diagonal, the row interchanges of ipiv first
+//               (L of the LU factors: entry 0 is the diagonal, e the row j+e);
+//   kRingBwd    positions reversed (position q is row n-1-q), x_j = b_j / entry K,
+//               entry K-d updates the row d above (U with kv superdiagonals);
+//   kRingFwdDiv forward, x_j = b_j / entry 0, no interchanges (a lower
+//               triangular matrix with its diagonal).
 //
 // Wave 0 holds the right-hand side window in registers: slot s of lane L is
 // position 64(B+s)+L while the steps of block B = j/64 run, C = Q+2 slots for
@@ -40,12 +47,16 @@ constexpr int kPadLo = 128;        // LDS doubles before the buffers
 constexpr int kPadHi = 128;        // and after
 constexpr int kMaxQ = 15;          // K <= 1023
 
+enum { kRingFwdLU = 0, kRingBwd = 1, kRingFwdDiv = 2 };
+
 struct RingParams {
     const double *AB;
     const int32_t *ipiv;
     double *B;
     int64_t ldab, strideAB, strideP, ldb, strideB;
-    int n, kl, kv, nrhs;
+    int64_t cb0, es;    // entry e of step j at cb0 + col*ldab + e*es
+    int n, kl, nrhs;    // kl: interchange reach (kRingFwdLU)
+    int K, nsteps;      // positions a step updates; steps in the pass
 };
 
 // steps per LDS half-buffer: both halves of LDC = 64(Q+1) doubles per column
@@ -67,8 +78,9 @@ __device__ __forceinline__ bool in_lanes(unsigned long long m) {
     return __builtin_amdgcn_inverse_ballot_w64(m);
 }
 
-template <int Q, bool BWD>
+template <int Q, int MODE>
 __global__ __launch_bounds__(kRingThreads) void getrs_ring_kernel(RingParams P) {
+    constexpr bool BWD = MODE == kRingBwd;
     constexpr int C = Q + 2;               // register slots of the window
     constexpr int NB = ring_nb<Q>();       // steps per LDS half-buffer
     constexpr int LDC = 64 * (Q + 1);      // LDS stride between columns (>= K + 1)
@@ -78,19 +90,19 @@ __global__ __launch_bounds__(kRingThreads) void getrs_ring_kernel(RingParams P) 
     const int tid = threadIdx.x;
     const int64_t sys = blockIdx.x;
     const int64_t bidx = sys / P.nrhs, krhs = sys - bidx * P.nrhs;
-    const int n = P.n, kv = P.kv, ldab = int(P.ldab);
-    const int K = BWD ? kv : P.kl;
-    const int nsteps = BWD ? n : n - 1;
+    const int n = P.n, ldab = int(P.ldab);
+    const int K = P.K;
+    const int nsteps = P.nsteps;
     const int nblk = (nsteps + NB - 1) / NB;
     const Buf ab = make_buf(P.AB + bidx * P.strideAB, uint32_t(int64_t(ldab) * n * 8));
 
     if (tid >= 64) {
         // ---------------------------------------------------- column staging --
-        // Column of step j: forward j (entries kv + e, e = 0..kl: the diagonal
-        // and the multipliers), backward n-1-j (entries e = 0..kv: U(col-kv+e, col)).
+        // Entries of step j: col = j forward, n-1-j backward; entry e at
+        // cb0 + col*ldab + e*es (outside the band: read as zero, never used)
         constexpr int E = (LDC + kLoaders - 1) / kLoaders;  // entries per thread per column
         const int lt = tid - 64;
-        const int g0 = BWD ? 0 : kv;
+        const int64_t band = int64_t(ldab) * n;
         auto stage = [&](int k) {
             double v[NB][E];
 #pragma unroll
@@ -100,8 +112,9 @@ __global__ __launch_bounds__(kRingThreads) void getrs_ring_kernel(RingParams P) 
 #pragma unroll
                 for (int i = 0; i < E; ++i) {
                     const int e = lt + kLoaders * i;
-                    const bool ok = j < nsteps && e <= K;
-                    v[c][i] = buf_ld(ab, ok ? uint32_t(col * ldab + g0 + e) * 8u : kOutside);
+                    const int64_t off = P.cb0 + int64_t(col) * ldab + int64_t(e) * P.es;
+                    const bool ok = j < nsteps && e <= K && off >= 0 && off < band;
+                    v[c][i] = buf_ld(ab, ok ? uint32_t(off) * 8u : kOutside);
                 }
             }
             double *dst = lds + kPadLo + (k & 1) * HALF;
@@ -134,7 +147,7 @@ __global__ __launch_bounds__(kRingThreads) void getrs_ring_kernel(RingParams P) 
     for (int s = 0; s < C; ++s) b[s] = buf_ld(xb, xoff(64 * s + L));
     double nxt = buf_ld(xb, xoff(64 * C + L));
     int ipv = 0, ipv_next = 0;
-    if constexpr (!BWD) {
+    if constexpr (MODE == kRingFwdLU) {
         ipv = buf_ld_i32(pb, L < n ? uint32_t(L) * 4u : kOutside);
         ipv_next = buf_ld_i32(pb, 64 + L < n ? uint32_t(64 + L) * 4u : kOutside);
     }
@@ -154,7 +167,7 @@ __global__ __launch_bounds__(kRingThreads) void getrs_ring_kernel(RingParams P) 
     int k = 0;           // LDS blocks entered
     bool live = nsteps > 0;
     double m[C];         // the step's factor entries by slot
-    double dg = 0.0;     // backward: U(j, j)
+    double dg = 0.0;     // dividing modes: the diagonal entry of the step
     uint32_t vhalf = 0;  // byte address of this lane's part in the current half
 
     auto fetch = [&]<int U>() __attribute__((always_inline)) {
@@ -166,9 +179,11 @@ __global__ __launch_bounds__(kRingThreads) void getrs_ring_kernel(RingParams P) 
             const int off = BWD ? (c * LDC + 64 * (C - 1 - s) + U) : (c * LDC + 64 + 64 * s - U);
             m[s] = *reinterpret_cast<const double *>(reinterpret_cast<const char *>(lds) + vhalf + off * 8);
         }
-        if constexpr (BWD) {
+        if constexpr (MODE == kRingBwd) {
             // the diagonal entry e = K of the column (uniform address)
             dg = lds[kPadLo + (((k - 1) & 1) * HALF) + c * LDC + K];
+        } else if constexpr (MODE == kRingFwdDiv) {
+            dg = lds[kPadLo + (((k - 1) & 1) * HALF) + c * LDC];
         }
     };
 
@@ -190,7 +205,7 @@ __global__ __launch_bounds__(kRingThreads) void getrs_ring_kernel(RingParams P) 
                         fetch.template operator()<u>();
                     }
                     double xj;
-                    if constexpr (BWD) {
+                    if constexpr (MODE != kRingFwdLU) {
                         const double z = b[0] / dg;
                         xj = readlane_d(z, u);
                         if (in_lanes(onehot)) b[0] = xj;
@@ -244,7 +259,7 @@ __global__ __launch_bounds__(kRingThreads) void getrs_ring_kernel(RingParams P) 
                         for (int s = 0; s + 1 < C; ++s) b[s] = b[s + 1];
                         b[C - 1] = nxt;
                         nxt = buf_ld(xb, xoff(B0 + 64 * (C + 1) + L));
-                        if constexpr (!BWD) {
+                        if constexpr (MODE == kRingFwdLU) {
                             ipv = ipv_next;
                             const int pi = B0 + 128 + L;
                             ipv_next = buf_ld_i32(pb, pi < n ? uint32_t(pi) * 4u : kOutside);
@@ -270,18 +285,18 @@ __global__ __launch_bounds__(kRingThreads) void getrs_ring_kernel(RingParams P) 
 
 typedef void (*RingLaunch)(const RingParams &P, int64_t systems, hipStream_t s);
 
-template <int Q, bool BWD>
+template <int Q, int MODE>
 void ring_launch(const RingParams &P, int64_t systems, hipStream_t s) {
-    hipLaunchKernelGGL((getrs_ring_kernel<Q, BWD>), dim3((unsigned)systems), dim3(kRingThreads), 0,
+    hipLaunchKernelGGL((getrs_ring_kernel<Q, MODE>), dim3((unsigned)systems), dim3(kRingThreads), 0,
                        s, P);
 }
 
 // launchers of one pass for Q in [LO, HI] (one translation unit per range)
-template <bool BWD, int LO, int HI>
+template <int MODE, int LO, int HI>
 RingLaunch ring_launcher(int q) {
     RingLaunch f = nullptr;
     [&]<int... Is>(std::integer_sequence<int, Is...>) {
-        ((q == LO + Is ? (f = &ring_launch<LO + Is, BWD>, 0) : 0), ...);
+        ((q == LO + Is ? (f = &ring_launch<LO + Is, MODE>, 0) : 0), ...);
     }(std::make_integer_sequence<int, HI - LO + 1>{});
     return f;
 }
@@ -290,5 +305,15 @@ RingLaunch ring_launcher_fwd_0_7(int q);
 RingLaunch ring_launcher_fwd_8_15(int q);
 RingLaunch ring_launcher_bwd_0_7(int q);
 RingLaunch ring_launcher_bwd_8_15(int q);
+RingLaunch ring_launcher_div_0_7(int q);
+RingLaunch ring_launcher_div_8_15(int q);
+
+// one pass of the chain for any K <= 1023 (the launcher for K's register group)
+inline RingLaunch ring_pass(int mode, int K) {
+    const int q = K >> 6;
+    if (mode == kRingFwdLU) return q < 8 ? ring_launcher_fwd_0_7(q) : ring_launcher_fwd_8_15(q);
+    if (mode == kRingBwd) return q < 8 ? ring_launcher_bwd_0_7(q) : ring_launcher_bwd_8_15(q);
+    return q < 8 ? ring_launcher_div_0_7(q) : ring_launcher_div_8_15(q);
+}
 
 }  // namespace bandlu

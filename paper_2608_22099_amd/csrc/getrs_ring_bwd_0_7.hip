@@ -4,6 +4,6 @@
 
 namespace bandlu {
 
-RingLaunch ring_launcher_bwd_0_7(int q) { return ring_launcher<true, 0, 7>(q); }
+RingLaunch ring_launcher_bwd_0_7(int q) { return ring_launcher<kRingBwd, 0, 7>(q); }
 
 }  // namespace bandlu

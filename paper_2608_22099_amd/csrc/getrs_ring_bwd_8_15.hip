@@ -4,6 +4,6 @@
 
 namespace bandlu {
 
-RingLaunch ring_launcher_bwd_8_15(int q) { return ring_launcher<true, 8, 15>(q); }
+RingLaunch ring_launcher_bwd_8_15(int q) { return ring_launcher<kRingBwd, 8, 15>(q); }
 
 }  // namespace bandlu

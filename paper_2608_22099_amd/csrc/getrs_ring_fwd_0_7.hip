@@ -4,6 +4,6 @@
 
 namespace bandlu {
 
-RingLaunch ring_launcher_fwd_0_7(int q) { return ring_launcher<false, 0, 7>(q); }
+RingLaunch ring_launcher_fwd_0_7(int q) { return ring_launcher<kRingFwdLU, 0, 7>(q); }
 
 }  // namespace bandlu

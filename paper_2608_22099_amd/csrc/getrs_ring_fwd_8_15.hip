@@ -4,6 +4,6 @@
 
 namespace bandlu {
 
-RingLaunch ring_launcher_fwd_8_15(int q) { return ring_launcher<false, 8, 15>(q); }
+RingLaunch ring_launcher_fwd_8_15(int q) { return ring_launcher<kRingFwdLU, 8, 15>(q); }
 
 }  // namespace bandlu

@@ -243,7 +243,7 @@ class DenseLU:
         return B
 
 
-def structure_aware_lu(A, model=None, caps=None):
+def structure_aware_lu(A, model=None, caps=None, fused_caps=None):
     """Listing 2 on the GPU.
 
     A is an (n, lda) float64 device tensor holding the column-major matrix
@@ -252,8 +252,23 @@ def structure_aware_lu(A, model=None, caps=None):
     host in the path's one device-to-host copy.  If the speedup constraint
     holds the matrix is converted and factored with the banded LU (BandLU);
     otherwise it is factored densely with rocSOLVER (DenseLU).
+
+    ``fused_caps`` = (kl_cap, ku_cap) takes the fused identify-and-convert
+    pass instead: one read of the dense matrix packs the band of those caps
+    while it detects (an (n, 2 kl_cap + ku_cap + 1) array), and the banded LU
+    runs on the view of the detected band inside it.  If a cap is exceeded the
+    path falls back to detection with the policy's caps.
     """
     n = A.shape[0]
+    if fused_caps is not None:
+        fkl, fku = (min(max(c, 0), max(n - 1, 0)) for c in fused_caps)
+        out, ABc = bandlu.band_detect_convert(A, fkl, fku)
+        kl, ku, exceeded = (int(v) for v in out.cpu())  # the one device->host copy
+        if not exceeded and speedup_predicate(n, kl, ku, model):
+            AB = bandlu.band_view(ABc, fkl, fku, kl, ku)
+            ipiv, info = bandlu.band_getrf(AB, kl, ku)
+            return BandLU(AB, kl, ku, ipiv, info)
+        del ABc
     kl_cap, ku_cap = band_caps(n, model) if caps is None else caps
     out = bandlu.band_detect(A, kl_cap, ku_cap)
     kl, ku, exceeded = (int(v) for v in out.cpu())  # the one device->host copy
@@ -263,6 +278,42 @@ def structure_aware_lu(A, model=None, caps=None):
         return BandLU(AB, kl, ku, ipiv, info)
     LU, piv = torch.linalg.lu_factor(A[:, :n].transpose(0, 1))
     return DenseLU(LU, piv, kl, ku, exceeded)
+
+
+# ------------------------------------------------------- Listing 1 on GPU --
+def structure_aware_solve(A, B, model=None, caps=None, spd=True):
+    """The backslash dispatch of Listing 1 (Sec. I-C) on the GPU: solve
+    A X = B in place on B (shape (nrhs, ldb), ``B[k, i]`` = row i of column k).
+
+    Detection (with the caps of ``band_caps``) decides the branch, as
+    Listing 1's element inspection does:
+      * ku = 0 and/or kl = 0: diagonal, lower or upper triangular -- the band
+        is converted and solved by substitution (band_trsv), no factorisation;
+      * kl = ku and the band symmetric (``spd``): band Cholesky, the
+        Cholesky case the paper names beside LU (Sec. II-B); a matrix that
+        turns out not to be positive definite falls back to the LU branch;
+      * otherwise, when the speedup constraint holds: banded LU and solve
+        (Listing 2's branch), else the dense LU (rocSOLVER through torch).
+    Returns the name of the branch taken."""
+    n = A.shape[0]
+    kl_cap, ku_cap = band_caps(n, model) if caps is None else caps
+    out = bandlu.band_detect(A, kl_cap, ku_cap)
+    kl, ku, exceeded = (int(v) for v in out.cpu())  # the one device->host copy
+    if not exceeded and (kl == 0 or ku == 0):
+        AB = bandlu.dense_to_band(A, kl, ku)
+        bandlu.band_trsv(AB, kl, ku, B)
+        return "diagonal" if kl == ku else ("upper" if kl == 0 else "lower")
+    if not exceeded and spd and kl == ku and speedup_predicate(n, kl, ku, model):
+        if int(bandlu.band_is_symmetric(A, kl).cpu()[0]):
+            ABc = bandlu.dense_to_band(A, kl, 0)
+            low = ABc[:, kl:]  # LAPACK's lower layout inside the converted band
+            info = int(bandlu.band_pbtrf(low, kl).cpu()[0])
+            if info == 0:
+                bandlu.band_pbtrs(low, kl, B)
+                return "cholesky"
+    f = structure_aware_lu(A, model=model, caps=(kl_cap, ku_cap))
+    f.solve(B)
+    return f.branch
 
 
 def timed_slowdown(A, model=None, reps=3):

@@ -79,6 +79,29 @@ def test_argument_validation(lib):
     assert b"noalloc" in lib.band_last_error()
     assert lib.band_getrs(10, 2, 3, -1, fake, 8, fake, fake, 10, None) == -4
     assert lib.band_getrs(10, 2, 3, 1, fake, 8, fake, fake, 9, None) == -9
+    # the branches beyond the LU path validate on the host too
+    L = lib
+    i64, vp = ctypes.c_int64, ctypes.c_void_p
+    L.band_trsv.argtypes = [i64, i64, i64, i64, vp, i64, vp, i64, vp, vp]
+    L.band_getrs_t.argtypes = [i64, i64, i64, i64, vp, i64, vp, vp, i64, vp]
+    L.band_getrf_mn.argtypes = [i64, i64, i64, i64, vp, i64, vp, vp, vp]
+    L.band_pbtrf.argtypes = [i64, i64, vp, i64, vp, vp]
+    L.band_pbtrs.argtypes = [i64, i64, i64, vp, i64, vp, i64, vp]
+    L.band_is_symmetric.argtypes = [vp, i64, i64, i64, vp, vp]
+    L.band_detect_convert.argtypes = [vp, i64, i64, i64, i64, vp, vp, i64, vp]
+    assert L.band_trsv(10, 2, 3, 1, fake, 8, fake, 10, fake, None) == -3  # not triangular
+    assert L.band_trsv(10, 2, 0, 1, fake, 4, fake, 10, fake, None) == -6
+    assert L.band_trsv(10, 0, 2, 1, fake, 3, fake, 9, fake, None) == -8
+    assert L.band_getrs_t(10, 2, 3, 1, fake, 7, fake, fake, 10, None) == -6
+    assert L.band_getrf_mn(5, 10, 5, 2, fake, 20, fake, fake, None) == -3  # kl > m-1
+    assert L.band_getrf_mn(5, 10, 2, 10, fake, 20, fake, fake, None) == -4
+    assert L.band_getrf_mn(5, 10, 2, 3, fake, 7, fake, fake, None) == -6
+    assert L.band_pbtrf(10, 3, fake, 3, fake, None) == -4
+    assert L.band_pbtrf(10, 10, fake, 11, fake, None) == -2
+    assert L.band_pbtrs(10, 3, 1, fake, 4, fake, 9, None) == -7
+    assert L.band_is_symmetric(fake, 10, 9, 2, fake, None) == -3
+    assert L.band_detect_convert(fake, 10, 10, -1, 2, fake, fake, 10, None) == -4
+    assert L.band_detect_convert(fake, 10, 10, 2, 2, fake, fake, 6, None) == -8
     # band_getrf_ex: argument 11 is the variant; a variant that cannot take the
     # sizes is refused before anything is enqueued
     assert lib.band_getrf_ex(10, 2, 3, fake, 8, 80, fake, 10, fake, 1, 9, None) == -11

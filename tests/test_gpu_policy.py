@@ -113,3 +113,84 @@ def test_cost_model_and_slowdown():
     assert 1.0 <= s["slowdown"] <= s["slowdown_full_scan"] + 0.05
     res = policy.structure_aware_lu(A, model=model)
     assert res.branch == "dense"
+
+
+# ------------------------------------------------ Listing 1's dispatch --
+def _sym(n, kd, seed):
+    rng = np.random.default_rng(seed)
+    A = np.zeros((n, n))
+    for d in range(1, kd + 1):
+        v = rng.standard_normal(n - d)
+        A[np.arange(d, n), np.arange(n - d)] = v
+        A[np.arange(n - d), np.arange(d, n)] = v
+    A[np.arange(n), np.arange(n)] = np.abs(A).sum(0) + 1.0
+    return A
+
+
+@pytest.mark.parametrize("case", ["diagonal", "lower", "upper", "cholesky", "banded", "indefinite"])
+def test_structure_aware_solve_branches(case):
+    """Each branch of the backslash dispatch gives the oracle's solution bit
+    for bit (the triangular solve, the band Cholesky, the band LU)."""
+    n = 3000
+    rng = np.random.default_rng(3100)
+    if case == "diagonal":
+        T, kl, ku = inputs.banded_dense(n, 0, 0, 3101, shift=2.0), 0, 0
+    elif case == "lower":
+        T, kl, ku = inputs.banded_dense(n, 7, 0, 3102, shift=16.0), 7, 0
+    elif case == "upper":
+        T, kl, ku = inputs.banded_dense(n, 0, 40, 3103, shift=80.0), 0, 40
+    elif case == "banded":
+        T, kl, ku = inputs.banded_dense(n, 5, 9, 3104), 5, 9
+    else:
+        A = _sym(n, 6, 3105)
+        if case == "indefinite":
+            A[1000, 1000] = -1.0
+        T, kl, ku = np.ascontiguousarray(A.T), 6, 6
+    b = rng.standard_normal((2, n))
+    B = torch.from_numpy(b.copy()).to(DEV)
+    branch = policy.structure_aware_solve(torch.from_numpy(T).to(DEV), B)
+    got = B.cpu().numpy()
+    expect = {"indefinite": "banded"}.get(case, case)
+    assert branch == expect
+    ref = b.copy()
+    if case in ("diagonal", "lower", "upper"):
+        AB, _ = oracle.dense_to_band(T, kl, ku)
+        oracle.band_trsv(AB, kl, ku, ref)
+    elif case == "cholesky":
+        AB = oracle.lower_band(T.T.copy(), kl)
+        assert oracle.pbtrf(AB, kl) == 0
+        oracle.pbtrs(AB, kl, ref)
+    else:
+        AB, _ = oracle.dense_to_band(T, kl, ku)
+        ipo, _, _ = oracle.gbtrf(AB, kl, ku)
+        oracle.gbtrs(AB, kl, ku, ipo, ref)
+    assert np.array_equal(bits(got), bits(ref))
+
+
+def test_structure_aware_solve_dense():
+    n = 600
+    T = np.random.default_rng(3200).standard_normal((n, n))
+    b = np.random.default_rng(3201).standard_normal((1, n))
+    B = torch.from_numpy(b.copy()).to(DEV)
+    assert policy.structure_aware_solve(torch.from_numpy(T).to(DEV), B) == "dense"
+    x = B.cpu().numpy()[0]
+    r = T.T @ x - b[0]
+    assert np.abs(r).max() < 1e-9 * np.abs(T).sum(0).max() * max(1.0, np.abs(x).max())
+
+
+@pytest.mark.parametrize("name", ["n8192_kl16_ku16", "n16384_kl2_ku64"])
+def test_structure_aware_lu_fused(name):
+    """The fused identify-and-convert pass feeds the band LU the same band as
+    the two separate steps: factors and pivots equal the oracle's bit for bit."""
+    w = inputs.WORKLOADS[name]
+    n, kl, ku = w["n"], w["kl"], w["ku"]
+    T = inputs.workload_matrix(name)
+    res = policy.structure_aware_lu(torch.from_numpy(T).to(DEV), fused_caps=(kl + 8, ku + 8))
+    assert res.branch == "banded" and (res.kl, res.ku) == (kl, ku)
+    ABo, _ = oracle.dense_to_band(T, kl, ku)
+    ipo, info_o, _ = oracle.gbtrf(ABo, kl, ku)
+    assert np.array_equal(res.ipiv.cpu().numpy(), ipo)
+    assert np.array_equal(bits(res.AB.cpu().numpy()), bits(ABo))
+    # caps below the bandwidths: falls back to the two separate steps
+    res2 = policy.structure_aware_lu(torch.from_numpy(T).to(DEV), fused_caps=(kl - 1, ku))
+    assert res2.branch == "banded" and np.array_equal(res2.ipiv.cpu().numpy(), ipo)
