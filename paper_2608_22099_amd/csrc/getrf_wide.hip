@@ -397,21 +397,27 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
         };
         // step S in wave 0: lane S's row is final; it writes the row and its
         // reciprocal to row S of sU (the buffer waves 1..4 read after the
-        // group's barrier) and every lane reads them back at once (the LDS
-        // operations of one wave complete in order)
+        // group's barrier; one 8-byte store per entry, straight from its
+        // register, as a paired store would first copy both into adjacent
+        // registers), and every lane reads the row back at once (the LDS
+        // operations of one wave complete in order).  The pivot and its
+        // reciprocal come from lane S by lane reads instead (uniform, so the
+        // branches on them are scalar; no LDS round trip on the chain).
         auto step_w0 = [&]<int S>() __attribute__((always_inline)) {
             if (S >= nbn) return;
             step_fence();
             double *us = sUb + S * LDU;
             if (lane == S) {
 #pragma unroll
-                for (int c = S; c < NB; ++c) us[c] = x[c];
+                for (int c = S; c < NB; ++c) {
+                    us[c] = x[c];
+                    step_fence();
+                }
                 us[NB] = r;
             }
             __builtin_amdgcn_wave_barrier();
-            // (the same in every lane: uniform, so the branches on it are scalar)
-            const double piv = uniform_d(us[S]);
-            const double rcp = uniform_d(us[NB]);
+            const double piv = readlane_d(x[S], S);
+            const double rcp = readlane_d(r, S);
             const int km = min(kl, n - 1 - (j0 + S));
             upd_row(x, myr, own, us, S, piv, rcp, km);
             if (piv == 0.0) {

@@ -102,19 +102,43 @@ __global__ __launch_bounds__(kRingThreads) void getrs_ring_kernel(RingParams P) 
         // cb0 + col*ldab + e*es (outside the band: read as zero, never used)
         constexpr int E = (LDC + kLoaders - 1) / kLoaders;  // entries per thread per column
         const int lt = tid - 64;
-        const int64_t band = int64_t(ldab) * n;
+        // (every offset inside the band fits 32 bits: the band is below 2 GiB;
+        // one unsigned compare rejects both ends)
+        const uint32_t band = uint32_t(ldab) * uint32_t(n);
+        const int esi = int(P.es), cb0 = int(P.cb0);
+        const int lt_es = lt * esi, step_es = kLoaders * esi;
+        // (a step's entries are consecutive in the common case es = 1, where
+        // every one of them lies inside the band: that case keeps constant
+        // offsets and no range check)
+        const bool unit = esi == 1;
         auto stage = [&](int k) {
             double v[NB][E];
+            if (unit) {
 #pragma unroll
-            for (int c = 0; c < NB; ++c) {
-                const int j = k * NB + c;
-                const int col = BWD ? n - 1 - j : j;
+                for (int c = 0; c < NB; ++c) {
+                    const int j = k * NB + c;
+                    const int col = BWD ? n - 1 - j : j;
+                    const int o0 = cb0 + col * ldab + lt;
 #pragma unroll
-                for (int i = 0; i < E; ++i) {
-                    const int e = lt + kLoaders * i;
-                    const int64_t off = P.cb0 + int64_t(col) * ldab + int64_t(e) * P.es;
-                    const bool ok = j < nsteps && e <= K && off >= 0 && off < band;
-                    v[c][i] = buf_ld(ab, ok ? uint32_t(off) * 8u : kOutside);
+                    for (int i = 0; i < E; ++i) {
+                        const int e = lt + kLoaders * i;
+                        const bool ok = j < nsteps && e <= K;
+                        v[c][i] = buf_ld(ab, ok ? uint32_t(o0 + kLoaders * i) * 8u : kOutside);
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int c = 0; c < NB; ++c) {
+                    const int j = k * NB + c;
+                    const int col = BWD ? n - 1 - j : j;
+                    const int o0 = cb0 + col * ldab + lt_es;
+#pragma unroll
+                    for (int i = 0; i < E; ++i) {
+                        const int e = lt + kLoaders * i;
+                        const uint32_t off = uint32_t(o0 + i * step_es);
+                        const bool ok = j < nsteps && e <= K && off < band;
+                        v[c][i] = buf_ld(ab, ok ? off * 8u : kOutside);
+                    }
                 }
             }
             double *dst = lds + kPadLo + (k & 1) * HALF;
