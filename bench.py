@@ -4,7 +4,11 @@ One step = the whole path of the paper's Listing 2 plus the solve, on one
 matrix (or one batch) of synthetic dense-stored banded input already resident
 in HBM: band_detect (with the early-exit caps of the speedup constraint) ->
 one device-to-host copy of (kl, ku, exceeded) -> host policy (Sec. II-B
-speedup constraint) -> dense_to_band -> band_getrf -> band_getrs.
+speedup constraint) -> dense_to_band -> band_getrf -> band_getrs.  A single
+matrix takes the two halves of band_gbsv for the last two (the same results:
+"getrf" is the factorisation with the forward half of the solve, fused into
+the persistent wide-band launch where that kernel runs, "getrs" the backward
+half); a batch calls band_getrf_batched and band_getrs_batched.
 
 Prints ONE JSON line.  `value` is factorizations per second of the whole
 path; per-call times come from HIP events on the stream every call is enqueued
@@ -57,13 +61,13 @@ STEP_SOURCES = {
     "convert": ["convert.hip", "common.hpp"],
     "getrf": ["getrf.hip", "getrf_win64.hpp", "getrf_win2.hpp", "getrf_window.hpp", "getrf_g16.hpp",
               "getrf_split.hpp", "getrf_diag.hpp", "getrf_blocked.hip", "getrf_mfma.hip",
-              "getrf_wide.hip", "wave.hpp", "bufio.hpp", "common.hpp"],
-    "getrs": ["getrs.hip", "getrs_ring.hpp", "getrs_ring.hip", "getrs_lane.hip", "bufio.hpp",
-              "common.hpp"],
+              "getrf_wide.hip", "chain.hip", "wave.hpp", "bufio.hpp", "common.hpp"],
+    "getrs": ["getrs.hip", "getrs_ring.hpp", "getrs_ring.hip", "getrs_lane.hip", "chain.hip",
+              "bufio.hpp", "common.hpp"],
 }
 # instantiation files of a step (one per parameter range), by name prefix
 STEP_PREFIXES = {"getrf": ("getrf_win_g", "getrf_split_c", "getrf_diag_ku"),
-                 "getrs": ("getrs_ring_fwd", "getrs_ring_bwd")}
+                 "getrs": ("getrs_ring_fwd", "getrs_ring_bwd", "getrs_ring_div")}
 
 
 def source_hash(step):
@@ -360,17 +364,20 @@ def main():
             bandlu.dense_to_band(A, kl_d, ku_d, AB=AB)
         else:
             bandlu.dense_to_band_batched(A, kl_d, ku_d, AB=AB)
+        x.copy_(b0)
         if timed:
             ev[3].record()
+        # one matrix: the factorisation with the forward half of the solve
+        # (fused into the persistent wide-band launch where that kernel runs),
+        # then the backward half -- band_getrf + band_getrs, the same results
         if batch == 1:
-            bandlu.band_getrf(AB, kl_d, ku_d, ipiv=ipiv, info=info)
+            bandlu.band_gbsv_lu(AB, kl_d, ku_d, x, ipiv=ipiv, info=info)
         else:
             bandlu.band_getrf_batched(AB, kl_d, ku_d, ipiv=ipiv, info=info)
         if timed:
             ev[4].record()
-        x.copy_(b0)
         if batch == 1:
-            bandlu.band_getrs(AB, kl_d, ku_d, ipiv, x)
+            bandlu.band_gbsv_back(AB, kl_d, ku_d, x)
         else:
             bandlu.band_getrs_batched(AB, kl_d, ku_d, ipiv, x)
         if timed:
@@ -417,6 +424,9 @@ def main():
         kernels[k]["algorithmic_bytes"] = costs[k]["bytes"]
     kernels["getrf"]["variant"] = variant
     kernels["getrs"]["variant"] = bandlu.band_getrs_variant(n, kl, ku, 1, batch)
+    if batch == 1:
+        kernels["getrf"]["entry"] = "band_gbsv_lu (factorisation + forward half of the solve)"
+        kernels["getrs"]["entry"] = "band_gbsv_back (backward half of the solve)"
 
     out = {
         "metric": METRIC, "value": value, "unit": "factorizations/s", "n_gpus": 1,

@@ -268,6 +268,29 @@ int band_getrs_ex(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double 
                   double *dB, int64_t ldb, int64_t strideB, int64_t batch, int variant,
                   void *stream);
 
+/*
+ * band_gbsv -- steps 3 and 4 in one call (xGBSV): band_getrf on dAB, then
+ * band_getrs on the nrhs columns of B (ldb >= n).  dAB, d_ipiv, *d_info and X
+ * are those of the two calls, bitwise.  It is band_gbsv_lu followed by
+ * band_gbsv_back:
+ *   - band_gbsv_lu: band_getrf, and the forward half of the solve,
+ *     B <- L^-1 P B.  When the persistent wide-band LU factors the matrix (see
+ *     band_getrf) and nrhs <= 33, the forward half runs inside that launch:
+ *     one more workgroup trails the chain of panels and applies each
+ *     published panel to the right-hand sides.  Otherwise the forward chain
+ *     runs after the factorisation.
+ *   - band_gbsv_back: the backward half, B <- U^-1 B, from the factors.
+ * As in band_getrs, B is solved even when *d_info > 0 (a zero pivot then
+ * gives IEEE infinities or NaN; LAPACK's xGBSV would skip the solve).
+ * Argument errors follow the order of each declaration.
+ */
+int band_gbsv(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, double *dAB, int64_t ldab,
+              int32_t *d_ipiv, double *dB, int64_t ldb, int32_t *d_info, void *stream);
+int band_gbsv_lu(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, double *dAB, int64_t ldab,
+                 int32_t *d_ipiv, double *dB, int64_t ldb, int32_t *d_info, void *stream);
+int band_gbsv_back(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *dAB,
+                   int64_t ldab, double *dB, int64_t ldb, void *stream);
+
 /* ----------------------------------------------------------------------
  * Beyond the LU path: the other branches and structures the paper points to
  * ---------------------------------------------------------------------- */

@@ -68,6 +68,9 @@ EXPORTS = {
     "band_pbtrf_batched": [_i64, _i64, _vp, _i64, _i64, _vp, _i64, _vp],
     "band_pbtrs": [_i64, _i64, _i64, _vp, _i64, _vp, _i64, _vp],
     "band_pbtrs_batched": [_i64, _i64, _i64, _vp, _i64, _i64, _vp, _i64, _i64, _i64, _vp],
+    "band_gbsv": [_i64, _i64, _i64, _i64, _vp, _i64, _vp, _vp, _i64, _vp, _vp],
+    "band_gbsv_lu": [_i64, _i64, _i64, _i64, _vp, _i64, _vp, _vp, _i64, _vp, _vp],
+    "band_gbsv_back": [_i64, _i64, _i64, _i64, _vp, _i64, _vp, _i64, _vp],
     "band_status_string": [ctypes.c_int],
     "band_last_error": [],
 }
@@ -483,4 +486,46 @@ def band_pbtrs_batched(AB, kd, B):
     sB = B.stride(0) if batch > 1 else ldb * nrhs
     _call("band_pbtrs_batched", n, kd, nrhs, _ptr(AB), ldab, sAB, _ptr(B), ldb, sB, batch,
           _stream())
+    return B
+
+
+# --------------------------------------------------- factor + solve (xGBSV) --
+def band_gbsv(AB, kl, ku, B, ipiv=None, info=None):
+    """band_getrf then band_getrs in one call (the forward substitution fused
+    into the persistent wide-band LU where that kernel runs); B (nrhs, ldb) is
+    overwritten with X.  Returns (ipiv, info)."""
+    _check(AB, torch.float64, "AB", 2)
+    _check(B, torch.float64, "B", 2)
+    n = AB.shape[0]
+    if ipiv is None:
+        ipiv = torch.empty(n, dtype=torch.int32, device=AB.device)
+    if info is None:
+        info = torch.empty(1, dtype=torch.int32, device=AB.device)
+    _call("band_gbsv", n, kl, ku, B.shape[0], _ptr(AB), max(_ld(AB), 1), _ptr(ipiv), _ptr(B),
+          max(_ld(B), n, 1), _ptr(info), _stream())
+    return ipiv, info
+
+
+def band_gbsv_lu(AB, kl, ku, B, ipiv=None, info=None):
+    """The first half of band_gbsv: band_getrf, and B <- L^-1 P B (inside the
+    persistent wide-band launch where it runs).  Returns (ipiv, info)."""
+    _check(AB, torch.float64, "AB", 2)
+    _check(B, torch.float64, "B", 2)
+    n = AB.shape[0]
+    if ipiv is None:
+        ipiv = torch.empty(n, dtype=torch.int32, device=AB.device)
+    if info is None:
+        info = torch.empty(1, dtype=torch.int32, device=AB.device)
+    _call("band_gbsv_lu", n, kl, ku, B.shape[0], _ptr(AB), max(_ld(AB), 1), _ptr(ipiv), _ptr(B),
+          max(_ld(B), n, 1), _ptr(info), _stream())
+    return ipiv, info
+
+
+def band_gbsv_back(AB, kl, ku, B):
+    """The second half of band_gbsv: B <- U^-1 B from the factors."""
+    _check(AB, torch.float64, "AB", 2)
+    _check(B, torch.float64, "B", 2)
+    n = AB.shape[0]
+    _call("band_gbsv_back", n, kl, ku, B.shape[0], _ptr(AB), max(_ld(AB), 1), _ptr(B),
+          max(_ld(B), n, 1), _stream())
     return B

@@ -26,6 +26,11 @@
 namespace bandlu {
 
 int launch_chain(int mode, const RingParams &P, int64_t batch, hipStream_t s);
+int launch_getrf_wide(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
+                      int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info,
+                      int64_t batch, hipStream_t s, void *scratch, size_t scratch_bytes,
+                      double *dB, int64_t ldb, int64_t strideB, int64_t nrhs);
+bool getrf_wide_fused_fits(int64_t n, int64_t kl, int64_t ku, int64_t nrhs);
 
 namespace {
 
@@ -48,11 +53,24 @@ __global__ __launch_bounds__(kAnyThreads) void chain_any_kernel(RingParams P) {
         for (int64_t i = tid; i < n; i += kAnyThreads) x[i] = Bg[i];
     }
     __syncthreads();
+    const int32_t *ipiv = MODE == kRingFwdLU ? P.ipiv + b * P.strideP : nullptr;
     for (int64_t j = 0; j < P.nsteps; ++j) {
         const int64_t col = BWD ? n - 1 - j : j;
         const int64_t rj = BWD ? n - 1 - j : j;
         const double *cb = AB + P.cb0 + col * ldab;
-        if (tid == 0) x[rj] = x[rj] / cb[(BWD ? K : 0) * P.es];
+        if (tid == 0) {
+            if constexpr (MODE == kRingFwdLU) {
+                // the row interchange of step j (unit diagonal: no division)
+                const int64_t l = ipiv[j] - 1;
+                if (l != j && l > j && l < n) {
+                    const double t0 = x[l];
+                    x[l] = x[j];
+                    x[j] = t0;
+                }
+            } else {
+                x[rj] = x[rj] / cb[(BWD ? K : 0) * P.es];
+            }
+        }
         __syncthreads();
         const double xj = x[rj];
         const int64_t dmax = std::min(K, n - 1 - j);
@@ -211,8 +229,12 @@ int launch_chain(int mode, const RingParams &P, int64_t batch, hipStream_t s) {
             hipLaunchKernelGGL((chain_any_kernel<kRingFwdDiv, false>), dim3((unsigned)systems),
                                dim3(kAnyThreads), 0, s, P);
     } else {
-        set_error("band chain: the interchange pass needs K <= 1023");
-        return BANDLU_ERR_UNSUPPORTED;
+        if (lds)
+            hipLaunchKernelGGL((chain_any_kernel<kRingFwdLU, true>), dim3((unsigned)systems),
+                               dim3(kAnyThreads), shm, s, P);
+        else
+            hipLaunchKernelGGL((chain_any_kernel<kRingFwdLU, false>), dim3((unsigned)systems),
+                               dim3(kAnyThreads), 0, s, P);
     }
     BANDLU_CHECK_LAUNCH("band chain (any band)");
     return BANDLU_OK;
@@ -414,4 +436,97 @@ extern "C" int band_getrs_t_batched(int64_t n, int64_t kl, int64_t ku, int64_t n
     }
     return getrs_t(n, kl, ku, nrhs, dAB, ldab, strideAB, d_ipiv, strideP, dB, ldb, strideB, batch,
                    as_stream(stream));
+}
+
+// Factor and solve (xGBSV) as two calls with one dominant kernel each:
+//   band_gbsv_lu:   band_getrf, and L y = P b on the right-hand sides (inside
+//                   the persistent wide-band launch when that kernel runs, in
+//                   a workgroup that trails the chain of panels; else the
+//                   forward chain after the factorisation);
+//   band_gbsv_back: U x = y, the backward chain.
+// band_gbsv is the two in turn.  The results are those of band_getrf and
+// band_getrs, bitwise.
+namespace bandlu {
+namespace {
+int gbsv_args(const char *fn, int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const void *dAB,
+              int64_t ldab, const void *d_ipiv, const void *dB, int64_t ldb) {
+    const int64_t bmax = n > 1 ? n - 1 : 0;
+    BANDLU_ARG(n >= 0, 1, "%s: n < 0", fn);
+    BANDLU_ARG(kl >= 0 && kl <= bmax, 2, "%s: kl out of [0, max(0, n-1)]", fn);
+    BANDLU_ARG(ku >= 0 && ku <= bmax, 3, "%s: ku out of [0, max(0, n-1)]", fn);
+    BANDLU_ARG(nrhs >= 0, 4, "%s: nrhs < 0", fn);
+    BANDLU_ARG(n == 0 || dAB != nullptr, 5, "%s: dAB is null", fn);
+    BANDLU_ARG(ldab >= 2 * kl + ku + 1, 6, "%s: ldab < 2kl+ku+1", fn);
+    BANDLU_ARG(n == 0 || d_ipiv != nullptr, 7, "%s: d_ipiv is null", fn);
+    BANDLU_ARG(n == 0 || nrhs == 0 || dB != nullptr, 8, "%s: dB is null", fn);
+    BANDLU_ARG(ldb >= (n > 1 ? n : 1), 9, "%s: ldb < max(1, n)", fn);
+    if (n > kMaxN || nrhs > INT_MAX) {
+        set_error("%s: sizes too large", fn);
+        return BANDLU_ERR_UNSUPPORTED;
+    }
+    return BANDLU_OK;
+}
+}  // namespace
+}  // namespace bandlu
+
+extern "C" int band_gbsv_lu(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, double *dAB,
+                            int64_t ldab, int32_t *d_ipiv, double *dB, int64_t ldb,
+                            int32_t *d_info, void *stream) {
+    clear_error();
+    if (int rc = gbsv_args("band_gbsv_lu", n, kl, ku, nrhs, dAB, ldab, d_ipiv, dB, ldb);
+        rc != BANDLU_OK)
+        return rc;
+    BANDLU_ARG(d_info != nullptr, 10, "band_gbsv_lu: d_info is null");
+    hipStream_t s = as_stream(stream);
+    if (n > 0 && nrhs > 0 && band_getrf_variant(n, kl, ku, 1) == BANDLU_GETRF_WIDE &&
+        getrf_wide_fused_fits(n, kl, ku, nrhs))
+        return launch_getrf_wide(n, kl, ku, dAB, ldab, ldab * n, d_ipiv, n, d_info, 1, s, nullptr,
+                                 0, dB, ldb, ldb * nrhs, nrhs);
+    if (int rc = band_getrf(n, kl, ku, dAB, ldab, d_ipiv, d_info, stream); rc != BANDLU_OK)
+        return rc;
+    if (n < 2 || nrhs == 0 || kl == 0) return BANDLU_OK;
+    RingParams P = chain_params(dAB, ldab, ldab * n, dB, ldb, ldb * nrhs, n, nrhs);
+    P.ipiv = d_ipiv;
+    P.strideP = n;
+    P.kl = (int)kl;
+    P.nsteps = (int)n - 1;
+    P.cb0 = kl + ku;
+    P.es = 1;
+    P.K = (int)kl;
+    return launch_chain(kRingFwdLU, P, 1, s);
+}
+
+extern "C" int band_gbsv_back(int64_t n, int64_t kl, int64_t ku, int64_t nrhs,
+                              const double *dAB, int64_t ldab, double *dB, int64_t ldb,
+                              void *stream) {
+    clear_error();
+    const int64_t bmax = n > 1 ? n - 1 : 0;
+    BANDLU_ARG(n >= 0, 1, "band_gbsv_back: n < 0");
+    BANDLU_ARG(kl >= 0 && kl <= bmax, 2, "band_gbsv_back: kl out of [0, max(0, n-1)]");
+    BANDLU_ARG(ku >= 0 && ku <= bmax, 3, "band_gbsv_back: ku out of [0, max(0, n-1)]");
+    BANDLU_ARG(nrhs >= 0, 4, "band_gbsv_back: nrhs < 0");
+    BANDLU_ARG(n == 0 || dAB != nullptr, 5, "band_gbsv_back: dAB is null");
+    BANDLU_ARG(ldab >= 2 * kl + ku + 1, 6, "band_gbsv_back: ldab < 2kl+ku+1");
+    BANDLU_ARG(n == 0 || nrhs == 0 || dB != nullptr, 7, "band_gbsv_back: dB is null");
+    BANDLU_ARG(ldb >= (n > 1 ? n : 1), 8, "band_gbsv_back: ldb < max(1, n)");
+    if (n > kMaxN || nrhs > INT_MAX) {
+        set_error("band_gbsv_back: sizes too large");
+        return BANDLU_ERR_UNSUPPORTED;
+    }
+    if (n == 0 || nrhs == 0) return BANDLU_OK;
+    RingParams P = chain_params(dAB, ldab, ldab * n, dB, ldb, ldb * nrhs, n, nrhs);
+    P.nsteps = (int)n;
+    P.cb0 = 0;
+    P.es = 1;
+    P.K = (int)(kl + ku);
+    return launch_chain(kRingBwd, P, 1, as_stream(stream));
+}
+
+extern "C" int band_gbsv(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, double *dAB,
+                         int64_t ldab, int32_t *d_ipiv, double *dB, int64_t ldb, int32_t *d_info,
+                         void *stream) {
+    if (int rc = band_gbsv_lu(n, kl, ku, nrhs, dAB, ldab, d_ipiv, dB, ldb, d_info, stream);
+        rc != BANDLU_OK)
+        return rc;
+    return band_gbsv_back(n, kl, ku, nrhs, dAB, ldab, dB, ldb, stream);
 }

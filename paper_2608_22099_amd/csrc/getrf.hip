@@ -95,7 +95,9 @@ int launch_getrf_mfma(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ld
                       int64_t batch, hipStream_t s);
 int launch_getrf_wide(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
                       int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info,
-                      int64_t batch, hipStream_t s, void *ws, size_t ws_bytes);
+                      int64_t batch, hipStream_t s, void *ws, size_t ws_bytes,
+                      double *dB = nullptr, int64_t ldb = 0, int64_t strideB = 0,
+                      int64_t nrhs = 0);
 bool getrf_wide_fits(int64_t n, int64_t kl, int64_t ku, int64_t batch);
 bool getrf_wide_one_launch(int64_t n, int64_t kl, int64_t ku, int64_t batch);
 size_t getrf_wide_scratch_bytes(int64_t n, int64_t kl, int64_t ku, int64_t batch);

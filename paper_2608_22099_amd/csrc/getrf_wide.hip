@@ -44,8 +44,10 @@ namespace bandlu {
 
 int launch_getrf_wide(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
                       int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info,
-                      int64_t batch, hipStream_t s, void *scratch, size_t scratch_bytes);
+                      int64_t batch, hipStream_t s, void *scratch, size_t scratch_bytes,
+                      double *dB, int64_t ldb, int64_t strideB, int64_t nrhs);
 bool getrf_wide_fits(int64_t n, int64_t kl, int64_t ku, int64_t batch);
+bool getrf_wide_fused_fits(int64_t n, int64_t kl, int64_t ku, int64_t nrhs);
 bool getrf_wide_one_launch(int64_t n, int64_t kl, int64_t ku, int64_t batch);
 size_t getrf_wide_scratch_bytes(int64_t n, int64_t kl, int64_t ku, int64_t batch);
 
@@ -77,6 +79,11 @@ struct WideParams {
     int n, kl, ku, nblk, G, nblocks;
     int b0;          // first matrix of this launch
     unsigned spin_limit;
+    // right-hand sides for the fused forward substitution (null: none); the
+    // workgroup after the G block owners applies each panel to them
+    double *B;
+    int64_t ldb, strideB;
+    int nrhs;
 };
 
 __device__ __forceinline__ int prow(int r) { return r % PR; }
@@ -120,6 +127,7 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
     char *scr = P.scratch + int64_t(blockIdx.y) * P.scratch_stride;
     int *counter = reinterpret_cast<int *>(scr);
     int *failed = counter + 1;
+    int *solved = counter + 2;  // panels the forward substitution has applied
     char *slots = scr + kHdrBytes;
     const int n = P.n, kl = P.kl, ku = P.ku, kv = kl + ku, G = P.G;
     const int64_t ldab = P.ldab;
@@ -161,6 +169,89 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         return s_ok != 0;
     };
+
+    // ------------------------------------------ forward substitution --
+    // L y = P b, the first half of the solve, trails the chain of panels in a
+    // workgroup of its own: for each published panel it applies the panel's
+    // net interchange, then y_top = L11^-1 b_top, then b_rest += (-L21) y_top
+    // to a window of 288 rows of the right-hand sides (row r of column q at
+    // W[prow(r) * LDW + q]).  Each value receives the fused multiply-adds of
+    // the column steps in their order, with the multipliers of those steps,
+    // so y is bitwise that of the unblocked forward pass.  It publishes how
+    // many panels it has applied, and a panel's slot is rewritten only after
+    // that (the owner of block b waits for panel b-G here before it factors).
+    if (P.B != nullptr && int(blockIdx.x) == G) {
+        double *Bm = P.B + int64_t(bm) * P.strideB;
+        const int nr = P.nrhs;
+        for (int idx = t; idx < PR * nr; idx += kThreads) {
+            const int q = idx / PR, w = idx - q * PR;
+            W[prow(w) * LDW + q] = w < n ? Bm[int64_t(q) * P.ldb + w] : 0.0;
+        }
+        __syncthreads();
+        for (int k = 0; k < P.nblocks; ++k) {
+            const int j0 = NB * k;
+            const int Rw = min(NB + kl, n - j0);
+            if (!wait_panel(k)) return;
+            const char *slot = slots + size_t(k % G) * kSlotBytes;
+            const int *sperm = reinterpret_cast<const int *>(slot);
+            const double *gL11 = reinterpret_cast<const double *>(slot + kSlotInts * 4);
+            const double *gNL = gL11 + NB * NB;
+            if (!sperm[PR]) {
+                // the panel's interchanges: one gather of whole rows
+                for (int q0 = 0; q0 < nr; q0 += 8) {
+                    double v[8];
+                    const bool mv = t < Rw;
+                    const int from = prow(j0 + (mv ? sperm[t] : 0)) * LDW;
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) v[q] = mv && q0 + q < nr ? W[from + q0 + q] : 0.0;
+                    __syncthreads();
+#pragma unroll
+                    for (int q = 0; q < 8; ++q)
+                        if (mv && q0 + q < nr) W[prow(j0 + t) * LDW + q0 + q] = v[q];
+                    __syncthreads();
+                }
+            }
+            // y_top = L11^-1 b_top, one thread per right-hand side (L11 unit
+            // lower, column-major: L11(r, s) at [s * 32 + r])
+            if (t < nr) {
+                double y[NB];
+#pragma unroll
+                for (int r = 0; r < NB; ++r) y[r] = W[prow(j0 + r) * LDW + t];
+#pragma unroll
+                for (int s2 = 0; s2 < NB - 1; ++s2)
+#pragma unroll
+                    for (int r = s2 + 1; r < NB; ++r) y[r] = __builtin_fma(-gL11[s2 * NB + r], y[s2], y[r]);
+#pragma unroll
+                for (int r = 0; r < NB; ++r) W[prow(j0 + r) * LDW + t] = y[r];
+            }
+            __syncthreads();
+            // rows 32..Rw-1 += (-L21) y_top, the steps in order
+            for (int idx = t; idx < (PR - NB) * nr; idx += kThreads) {
+                const int q = idx / (PR - NB), i = idx - q * (PR - NB);
+                if (NB + i < Rw) {
+                    double *bp = &W[prow(j0 + NB + i) * LDW + q];
+                    double acc = *bp;
+                    const int top = prow(j0) * LDW + q;
+#pragma unroll 8
+                    for (int s2 = 0; s2 < NB; ++s2)
+                        acc = __builtin_fma(gNL[s2 * (PR - NB) + i], W[top + s2 * LDW], acc);
+                    *bp = acc;
+                }
+            }
+            __syncthreads();
+            // rows j0..j0+31 are final; rows j0+288..j0+319 enter in their place
+            for (int idx = t; idx < NB * nr; idx += kThreads) {
+                const int q = idx / NB, i = idx - q * NB;
+                const int r = j0 + i;
+                double *wp = &W[prow(r) * LDW + q];
+                if (r < n) Bm[int64_t(q) * P.ldb + r] = *wp;
+                *wp = r + PR < n ? Bm[int64_t(q) * P.ldb + r + PR] : 0.0;
+            }
+            __syncthreads();
+            if (t == 0) __hip_atomic_store(solved, k + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        return;
+    }
 
     for (int b = blockIdx.x; b < P.nblocks; b += G) {
         const int cb = NB * b;
@@ -343,6 +434,23 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
         }
 
         // ------------------------------------------------ factor panel b --
+        // (with the fused forward substitution: the slot this panel takes is
+        // free once that workgroup has applied panel b-G)
+        if (P.B != nullptr && b >= G) {
+            if (t == 0) {
+                unsigned spins = 0;
+                while (__hip_atomic_load(solved, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < b - G + 1) {
+                    if (__hip_atomic_load(failed, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) break;
+                    if (++spins > P.spin_limit) {
+                        __hip_atomic_store(failed, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        __hip_atomic_store(info, INT_MIN, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(1);
+                }
+            }
+            __syncthreads();
+        }
         const int j0 = cb;
         const int nbn = min(NB, n - j0);
         const int Rn = min(nbn + kl, n - j0);
@@ -655,7 +763,7 @@ __global__ void wide_init_kernel(double *ABbase, int64_t ldab, int64_t strideAB,
             const int64_t c = e / kl, r = e - c * kl;
             if (r >= kv - c) AB[c * ldab + r] = 0.0;
         }
-        if (blockIdx.x == 0 && threadIdx.x < 2) {
+        if (blockIdx.x == 0 && threadIdx.x < 3) {
             if (threadIdx.x == 0) info[b0 + m] = 0;
             reinterpret_cast<int *>(scratch + int64_t(m) * scratch_stride)[threadIdx.x] = 0;
         }
@@ -716,10 +824,17 @@ bool getrf_wide_one_launch(int64_t n, int64_t kl, int64_t ku, int64_t batch) {
     return int64_t(wide_geom(n, kl, ku).G) * batch <= max_resident_groups();
 }
 
-// scratch one launch of the kernel needs (the matrices of a launch share it)
-static int64_t wide_chunk(int64_t n, int64_t kl, int64_t ku, int64_t batch) {
+// one matrix with the forward substitution fused: G + 1 co-resident
+// workgroups, and at most LDW right-hand sides in the window
+bool getrf_wide_fused_fits(int64_t n, int64_t kl, int64_t ku, int64_t nrhs) {
+    if (kl > kMaxKl || n > kMaxN || nrhs < 1 || nrhs > LDW) return false;
+    return wide_geom(n, kl, ku).G + 1 <= max_resident_groups();
+}
+
+// matrices per launch (the matrices of a launch share the scratch)
+static int64_t wide_chunk(int64_t n, int64_t kl, int64_t ku, int64_t batch, int extra = 0) {
     const WideGeom g = wide_geom(n, kl, ku);
-    return std::max<int64_t>(1, std::min<int64_t>(batch, max_resident_groups() / g.G));
+    return std::max<int64_t>(1, std::min<int64_t>(batch, max_resident_groups() / (g.G + extra)));
 }
 
 static int64_t wide_matrix_bytes(int64_t n, int64_t kl, int64_t ku) {
@@ -733,14 +848,18 @@ size_t getrf_wide_scratch_bytes(int64_t n, int64_t kl, int64_t ku, int64_t batch
 
 int launch_getrf_wide(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
                       int64_t strideAB, int32_t *d_ipiv, int64_t strideP, int32_t *d_info,
-                      int64_t batch, hipStream_t s, void *scratch, size_t scratch_bytes) {
-    if (!getrf_wide_fits(n, kl, ku, batch)) {
+                      int64_t batch, hipStream_t s, void *scratch, size_t scratch_bytes,
+                      double *dB, int64_t ldb, int64_t strideB, int64_t nrhs) {
+    const int extra = dB != nullptr ? 1 : 0;
+    if (!getrf_wide_fits(n, kl, ku, batch) ||
+        (extra && !getrf_wide_fused_fits(n, kl, ku, nrhs))) {
         set_error("band_getrf: the persistent wide-band variant needs kl <= %d and "
-                  "(kl+ku+31)/32 + 1 co-resident workgroups", kMaxKl);
+                  "(kl+ku+31)/32 + 1 co-resident workgroups (one more, and at most %d "
+                  "right-hand sides, with the fused forward substitution)", kMaxKl, LDW);
         return BANDLU_ERR_UNSUPPORTED;
     }
     const WideGeom g = wide_geom(n, kl, ku);
-    int64_t chunk = wide_chunk(n, kl, ku, batch);
+    int64_t chunk = wide_chunk(n, kl, ku, batch, extra);
     const int64_t per = wide_matrix_bytes(n, kl, ku);
     bool own_alloc = false;
     if (scratch == nullptr) {
@@ -774,6 +893,10 @@ int launch_getrf_wide(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ld
     P.G = g.G;
     P.nblocks = g.nblocks;
     P.spin_limit = spin_limit();
+    P.B = dB;
+    P.ldb = ldb;
+    P.strideB = strideB;
+    P.nrhs = (int)nrhs;
     int rc = BANDLU_OK;
     for (int64_t b0 = 0; b0 < batch; b0 += chunk) {
         const int cnt = (int)std::min<int64_t>(chunk, batch - b0);
@@ -789,7 +912,7 @@ int launch_getrf_wide(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ld
         P.b0 = (int)b0;
         void *args[] = {&P};
         if (hipError_t e = hipLaunchCooperativeKernel((const void *)getrf_wide_kernel,
-                                                      dim3((unsigned)g.G, (unsigned)cnt),
+                                                      dim3((unsigned)(g.G + extra), (unsigned)cnt),
                                                       dim3(kThreads), args, 0, s);
             e != hipSuccess) {
             rc = hip_fail(e, "band_getrf (wide-band persistent kernel)");

@@ -127,3 +127,86 @@ def test_wide_deterministic():
     a = run(T, 128, 100)
     b = run(T, 128, 100)
     assert np.array_equal(bits(a[0]), bits(b[0])) and np.array_equal(a[1], b[1])
+
+
+@pytest.mark.parametrize("n,kl,ku,nrhs,shift", [(2048, 256, 256, 1, 0.0), (3000, 64, 100, 3, 0.0),
+                                               (1500, 40, 30, 33, 40.0), (1000, 32, 0, 2, 0.0),
+                                               (1200, 100, 100, 34, 0.0), (700, 3, 3, 2, 0.0)])
+def test_gbsv_fused_equals_getrf_getrs(n, kl, ku, nrhs, shift):
+    """band_gbsv (the forward substitution fused into the persistent LU where
+    it runs: nrhs <= 33 on a wide band; else the two calls) gives exactly the
+    factors, pivots, info and solution of band_getrf + band_getrs."""
+    print(f"gbsv n={n} kl={kl} ku={ku} nrhs={nrhs}", flush=True)
+    T = inputs.banded_dense(n, kl, ku, 9900 + n + kl, shift=shift, check=False)
+    A = torch.from_numpy(T).to(DEV)
+    B = torch.from_numpy(np.random.default_rng(9901).standard_normal((nrhs, n))).to(DEV)
+    AB1 = bandlu.dense_to_band(A, kl, ku)
+    AB2 = AB1.clone()
+    B1, B2 = B.clone(), B.clone()
+    ip1, inf1 = bandlu.band_getrf(AB1, kl, ku)
+    bandlu.band_getrs(AB1, kl, ku, ip1, B1)
+    ip2, inf2 = bandlu.band_gbsv(AB2, kl, ku, B2)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(AB1.cpu().numpy()), bits(AB2.cpu().numpy()))
+    assert np.array_equal(ip1.cpu().numpy(), ip2.cpu().numpy())
+    assert int(inf1.cpu()[0]) == int(inf2.cpu()[0])
+    assert np.array_equal(bits(B1.cpu().numpy()), bits(B2.cpu().numpy()))
+    if shift:
+        # no interchange: the oracle's solution bit for bit
+        ABo, _ = oracle.dense_to_band(T, kl, ku)
+        ipo, _, _ = oracle.gbtrf(ABo, kl, ku)
+        xo = B.cpu().numpy().copy()
+        oracle.gbtrs(ABo, kl, ku, ipo, xo)
+        assert np.array_equal(bits(B2.cpu().numpy()), bits(xo))
+
+
+def test_gbsv_singular_and_workload():
+    """A zero column (info) and the n = 32768, kl = ku = 256 workload."""
+    n, kl, ku = 2000, 64, 64
+    T = inputs.banded_dense(n, kl, ku, 9950, check=False)
+    T[777, :] = 0.0
+    A = torch.from_numpy(T).to(DEV)
+    AB = bandlu.dense_to_band(A, kl, ku)
+    B = torch.ones((1, n), dtype=torch.float64, device=DEV)
+    ip, info = bandlu.band_gbsv(AB, kl, ku, B)
+    torch.cuda.synchronize()
+    ABo, _ = oracle.dense_to_band(T, kl, ku)
+    ipo, info_o, _ = oracle.gbtrf(ABo, kl, ku)
+    assert int(info.cpu()[0]) == info_o == 778 and np.array_equal(ip.cpu().numpy(), ipo)
+    name = "n32768_kl256_ku256"
+    w = inputs.WORKLOADS[name]
+    T = inputs.workload_matrix(name)
+    A = torch.from_numpy(T).to(DEV)
+    del T
+    AB1 = bandlu.dense_to_band(A, w["kl"], w["ku"])
+    del A
+    AB2 = AB1.clone()
+    b = torch.from_numpy(inputs.workload_rhs(name)).to(DEV)
+    B1, B2 = b.clone(), b.clone()
+    ip1, _ = bandlu.band_getrf(AB1, w["kl"], w["ku"])
+    bandlu.band_getrs(AB1, w["kl"], w["ku"], ip1, B1)
+    ip2, _ = bandlu.band_gbsv(AB2, w["kl"], w["ku"], B2)
+    torch.cuda.synchronize()
+    assert np.array_equal(ip1.cpu().numpy(), ip2.cpu().numpy())
+    assert torch.equal(AB1, AB2) and np.array_equal(bits(B1.cpu().numpy()), bits(B2.cpu().numpy()))
+
+
+@pytest.mark.parametrize("n,kl,ku", [(2048, 256, 256), (900, 5, 40), (1100, 1030, 1)])
+def test_gbsv_halves(n, kl, ku):
+    """band_gbsv_lu then band_gbsv_back: the fused wide path, the forward ring
+    after a narrow-band factorisation, and the any-band forward chain
+    (kl > 1023) -- each equal to band_getrf + band_getrs bit for bit."""
+    print(f"gbsv halves n={n} kl={kl} ku={ku}", flush=True)
+    T = inputs.banded_dense(n, kl, ku, 9970 + kl, check=False)
+    A = torch.from_numpy(T).to(DEV)
+    B = torch.from_numpy(np.random.default_rng(9971).standard_normal((2, n))).to(DEV)
+    AB1 = bandlu.dense_to_band(A, kl, ku)
+    AB2 = AB1.clone()
+    B1, B2 = B.clone(), B.clone()
+    ip1, inf1 = bandlu.band_getrf(AB1, kl, ku)
+    bandlu.band_getrs(AB1, kl, ku, ip1, B1)
+    ip2, inf2 = bandlu.band_gbsv_lu(AB2, kl, ku, B2)
+    bandlu.band_gbsv_back(AB2, kl, ku, B2)
+    torch.cuda.synchronize()
+    assert torch.equal(AB1, AB2) and torch.equal(ip1, ip2) and torch.equal(inf1, inf2)
+    assert np.array_equal(bits(B1.cpu().numpy()), bits(B2.cpu().numpy()))
