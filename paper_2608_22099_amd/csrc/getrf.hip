@@ -138,10 +138,10 @@ __global__ __launch_bounds__(kGenThreads) void getrf_generic_kernel(GenParams P)
 
     // in-matrix fill slots start at zero
     if (kl > 0) {
-        for (int64_t idx = tid; idx < n * kl; idx += kGenThreads) {
-            const int64_t c = idx / kl, r = idx - c * kl;
-            if (r >= kv - c && r - kv + c < m) AB[c * ldab + r] = 0.0;
-        }
+        // (columns by wavefront, fill rows by lane: no per-entry division)
+        for (int64_t c = wv; c < n; c += kGenThreads / 64)
+            for (int64_t r = lane; r < kl; r += 64)
+                if (r >= kv - c && r - kv + c < m) AB[c * ldab + r] = 0.0;
     }
     __syncthreads();
 
@@ -196,12 +196,14 @@ __global__ __launch_bounds__(kGenThreads) void getrf_generic_kernel(GenParams P)
             }
             __syncthreads();
             if (km > 0) {
-                const int64_t total = km * (ju - j);
-                for (int64_t idx = tid; idx < total; idx += kGenThreads) {
-                    const int64_t ci = idx / km, t = idx - ci * km + 1;
-                    const int64_t c = j + 1 + ci;
+                // columns j+1..ju by wavefront, rows by lane (no per-entry
+                // index division; one column's entries are contiguous)
+                constexpr int kGenWaves = kGenThreads / 64;
+                for (int64_t c = j + 1 + wv; c <= ju; c += kGenWaves) {
                     double *x = AB + c * ldab + (kv + j - c);  // x[0] = a(j, c)
-                    x[t] = __builtin_fma(-colj[t], x[0], x[t]);
+                    const double u = x[0];
+                    for (int64_t t = 1 + lane; t <= km; t += 64)
+                        x[t] = __builtin_fma(-colj[t], u, x[t]);
                 }
             }
             __syncthreads();
