@@ -10,7 +10,9 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "bandlu.h")
-LIB = os.path.join(ROOT, "paper_2608_22099_amd", "libbandlu.so")
+# (BANDLU_TEST_LIB: another build of the same library, e.g. one built with
+# the host code under a sanitizer)
+LIB = os.environ.get("BANDLU_TEST_LIB") or os.path.join(ROOT, "paper_2608_22099_amd", "libbandlu.so")
 
 
 def declared_functions():
