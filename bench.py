@@ -274,6 +274,85 @@ def early_exit_timings(torch, bandlu, A, n, kl, ku, caps):
     return res
 
 
+def extension_timings(torch, bandlu, A, n, kl, ku, ABf, ipf):
+    """The branches beyond the LU path on the same workload, each on the GPU:
+    the fused identify-and-convert pass against the two steps, the
+    transposed solve and the upper triangular solve with the timed factors,
+    a lower triangular band, band Cholesky and its solve on a symmetric
+    positive definite band of the same n, and a rectangular band LU.  In-place
+    calls get their inputs back before every rep, outside the timed region."""
+    dev = A.device
+
+    def timed(fn, restore=None, reps=5):
+        ts = []
+        for r in range(reps + 1):
+            if restore is not None:
+                restore()
+            torch.cuda.synchronize()
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            b.synchronize()
+            if r:
+                ts.append(a.elapsed_time(b))
+        return float(np.median(ts))
+
+    res = {}
+    g = torch.Generator(device=dev).manual_seed(321)
+    ldab = 2 * kl + ku + 1
+    # fused identify-and-convert, caps at the bandwidths (the view is the array)
+    out, out2 = (torch.empty(3, dtype=torch.int64, device=dev) for _ in range(2))
+    ABc = torch.empty((n, ldab), dtype=torch.float64, device=dev)
+    AB2 = torch.empty_like(ABc)
+    t_f = timed(lambda: bandlu.band_detect_convert(A, kl, ku, AB=ABc, out=out))
+    t_s = timed(lambda: (bandlu.band_detect(A, kl, ku, out=out2),
+                         bandlu.dense_to_band(A, kl, ku, AB=AB2)))
+    res["fused_detect_convert"] = {
+        "caps": [kl, ku], "ms": t_f, "separate_detect_plus_convert_ms": t_s,
+        "result": [int(v) for v in out.cpu()], "band_equal_to_separate": bool(torch.equal(ABc, AB2)),
+        "algorithmic_gbs": (8.0 * n * n + 8.0 * ldab * n) / (t_f * 1e-3) / 1e9}
+    del ABc, AB2
+    b = torch.randn((1, n), generator=g, dtype=torch.float64, device=dev)
+    x = torch.empty_like(b)
+    # transposed solve and the upper triangular solve (U of the factors as a
+    # band with kl = 0, ku = kl + ku) with the timed factors
+    res["getrs_t_ms"] = timed(lambda: bandlu.band_getrs_t(ABf, kl, ku, ipf, x),
+                              restore=lambda: x.copy_(b))
+    res["trsv_upper_ms"] = timed(lambda: bandlu.band_trsv(ABf, 0, kl + ku, x),
+                                 restore=lambda: x.copy_(b))
+    ABl = torch.randn((n, 2 * kl + 1), generator=g, dtype=torch.float64, device=dev)
+    ABl[:, kl] += 4.0 * (kl + 1)
+    res["trsv_lower_ms"] = timed(lambda: bandlu.band_trsv(ABl, kl, 0, x), restore=lambda: x.copy_(b))
+    del ABl
+    # band Cholesky on an SPD band (strictly diagonally dominant, lower layout)
+    for kd in (64, 140):
+        L0 = torch.randn((n, kd + 1), generator=g, dtype=torch.float64, device=dev)
+        L0[n - kd:, :] = 0.0
+        for d in range(1, kd + 1):
+            L0[n - d:, d] = 0.0
+        row = L0[:, 1:].abs().sum(1)
+        for d in range(1, kd + 1):
+            row[d:] += L0[:n - d, d].abs()
+        L0[:, 0] = row + 1.0
+        L = L0.clone()
+        info = torch.empty(1, dtype=torch.int32, device=dev)
+        t_f = timed(lambda: bandlu.band_pbtrf(L, kd, info=info), restore=lambda: L.copy_(L0))
+        t_s = timed(lambda: bandlu.band_pbtrs(L, kd, x), restore=lambda: x.copy_(b))
+        res[f"pbtrf_kd{kd}"] = {"n": n, "kd": kd, "ms": t_f, "info": int(info.cpu()[0]),
+                                "pbtrs_ms": t_s, "flops": float(n) * kd * (kd + 3)}
+        del L0, L
+    # rectangular band LU (one workgroup per matrix)
+    m2, n2, k2 = 9216, 8192, 16
+    R0 = torch.randn((n2, 3 * k2 + 1), generator=g, dtype=torch.float64, device=dev)
+    Rm = R0.clone()
+    res["getrf_mn"] = {"m": m2, "n": n2, "kl": k2, "ku": k2,
+                       "ms": timed(lambda: bandlu.band_getrf_mn(Rm, m2, k2, k2),
+                                   restore=lambda: Rm.copy_(R0))}
+    return res
+
+
 def slowdown_experiment(torch, policy, model, sizes=(8192, 16384, 32768)):
     """Sec. II-B slowdown on dense N(0,1) inputs: (I + F) / F with detection
     (early exit at the policy's caps, and as a full scan) in front of
@@ -454,6 +533,7 @@ def main():
             "speedup_constraint_op_counts": bool(policy.speedup_predicate(n, kl, ku))}
         if batch == 1:
             out["early_exit"] = early_exit_timings(torch, bandlu, A, n, kl, ku, caps)
+            out["extensions"] = extension_timings(torch, bandlu, A, n, kl, ku, AB, ipiv)
     if not args.no_dense and batch == 1:
         M = A[:, :n].transpose(0, 1)
         t_dense = event_ms(torch, lambda: torch.linalg.lu_factor(M), reps=3)

@@ -112,12 +112,17 @@ __global__ __launch_bounds__(64) void lt_swap_kernel(LtParams P) {
     int hi = n;                     // positions >= hi are stored back
     if (low + lane < n) ring[(low + lane) & mask] = x[low + lane];
     int ipv = 0, ipv_base = -1;
-    // multipliers of the next step's column, first 64 (prefetched a step ahead)
-    auto lcol = [&](int j) -> double {
+    // multipliers of the next step's column, the first kPre*64 (prefetched a
+    // step ahead, so that no step waits for a load)
+    constexpr int kPre = 4;
+    auto lcol = [&](int j, int ch) -> double {
         const int km = std::min(kl, n - 1 - j);
-        return (j >= 0 && 1 + lane <= km) ? AB[P.kv + 1 + lane + int64_t(j) * ldab] : 0.0;
+        const int t = 1 + 64 * ch + lane;
+        return (j >= 0 && t <= km) ? AB[P.kv + t + int64_t(j) * ldab] : 0.0;
     };
-    double lnext = lcol(n - 2);
+    double lnext[kPre];
+#pragma unroll
+    for (int ch = 0; ch < kPre; ++ch) lnext[ch] = lcol(n - 2, ch);
     __syncthreads();
     for (int j = n - 2; j >= 0; --j) {
         if (j < low) {
@@ -131,14 +136,31 @@ __global__ __launch_bounds__(64) void lt_swap_kernel(LtParams P) {
             ipv = ipv_base + lane <= j ? ipiv[ipv_base + lane] : 0;
         }
         const int km = std::min(kl, n - 1 - j);
-        double lv = lnext;
-        lnext = lcol(j - 1);
+        double lcur[kPre];
+#pragma unroll
+        for (int ch = 0; ch < kPre; ++ch) {
+            lcur[ch] = lnext[ch];
+            lnext[ch] = lcol(j - 1, ch);
+        }
         double acc = ring[j & mask];
-        for (int t0 = 1; t0 <= km; t0 += 64) {
-            if (t0 > 1) lv = 1 + (t0 - 1) + lane <= km ? AB[P.kv + t0 + lane + int64_t(j) * ldab] : 0.0;
+        for (int t0 = 1, ch = 0; t0 <= km; t0 += 64, ++ch) {
+            double lv = 0.0;
+#pragma unroll
+            for (int c2 = 0; c2 < kPre; ++c2)
+                if (ch == c2) lv = lcur[c2];
+            if (ch >= kPre) lv = lcol(j, ch);
             const double v = t0 + lane <= km ? ring[(j + t0 + lane) & mask] : 0.0;
             const int cnt = std::min(64, km - t0 + 1);
-            for (int u = 0; u < cnt; ++u) acc = __builtin_fma(-readlane_d(lv, u), readlane_d(v, u), acc);
+            // (the chain of fused multiply-adds in the order of the definition;
+            // unrolled by eight so that the lane reads of the next terms issue
+            // while an fma waits)
+            for (int u0 = 0; u0 < cnt; u0 += 8) {
+#pragma unroll
+                for (int u1 = 0; u1 < 8; ++u1) {
+                    const int u = u0 + u1;
+                    if (u < cnt) acc = __builtin_fma(-readlane_d(lv, u), readlane_d(v, u), acc);
+                }
+            }
         }
         const int p = __builtin_amdgcn_readlane(ipv, j - ipv_base) - 1;
         if (lane == 0) {

@@ -135,6 +135,9 @@ __global__ __launch_bounds__(kThreads) void detect_kernel(DetectParams P) {
                 const dbl2 *c2 = reinterpret_cast<const dbl2 *>(col);
                 const int n2 = int(n >> 1);
                 for (int base = 0; base < n2; base += 64 * kUnroll) {
+                    // (rows 2base..2base+128kUnroll-1 meet the caps' band?)
+                    const bool pk_here = PACK && 2 * base <= int(j) + P.pk.pkl &&
+                                         2 * (base + 64 * kUnroll) - 1 >= int(j) - P.pk.pku;
                     dbl2 v[kUnroll];
 #pragma unroll
                     for (int u = 0; u < kUnroll; ++u) {
@@ -146,7 +149,7 @@ __global__ __launch_bounds__(kThreads) void detect_kernel(DetectParams P) {
                         int i0 = 2 * (base + u * 64 + lane);
                         if (v[u].x != 0.0) { last = i0; first = min(first, i0); }
                         if (v[u].y != 0.0) { last = i0 + 1; first = min(first, i0 + 1); }
-                        if (PACK && base + u * 64 + lane < n2) {
+                        if (pk_here && base + u * 64 + lane < n2) {
                             pack_store<PACK>(P.pk, b, i0, int(j), v[u].x);
                             pack_store<PACK>(P.pk, b, i0 + 1, int(j), v[u].y);
                         }
@@ -160,6 +163,8 @@ __global__ __launch_bounds__(kThreads) void detect_kernel(DetectParams P) {
             } else {
                 const int nn = int(n);
                 for (int base = 0; base < nn; base += 64 * kUnroll) {
+                    const bool pk_here = PACK && base <= int(j) + P.pk.pkl &&
+                                         base + 64 * kUnroll - 1 >= int(j) - P.pk.pku;
                     double v[kUnroll];
 #pragma unroll
                     for (int u = 0; u < kUnroll; ++u) {
@@ -170,7 +175,7 @@ __global__ __launch_bounds__(kThreads) void detect_kernel(DetectParams P) {
                     for (int u = 0; u < kUnroll; ++u) {
                         int i0 = base + u * 64 + lane;
                         if (v[u] != 0.0) { last = i0; first = min(first, i0); }
-                        if (PACK && i0 < nn) pack_store<PACK>(P.pk, b, i0, int(j), v[u]);
+                        if (pk_here && i0 < nn) pack_store<PACK>(P.pk, b, i0, int(j), v[u]);
                     }
                 }
             }
@@ -253,6 +258,17 @@ __global__ __launch_bounds__(kThreads) void detect_flat_kernel(FlatParams P) {
         }
         const int64_t f0 = k * kFlatChunk;
         const int64_t fm = BATCHED ? f0 - mat * P.n * P.n : f0;  // offset inside the matrix
+        // the chunk [fm, fm + chunk) meets the caps' band, i.e. some column c
+        // has c (n+1) in [fm - pkl, fm + chunk - 1 + pku] (element (i, c) is at
+        // c n + i, and -pku <= i - c <= pkl)
+        bool pk_here = false;
+        if constexpr (PACK) {
+            const int64_t lo = fm - P.pk.pkl, hi = fm + kFlatChunk - 1 + P.pk.pku;
+            const int64_t np1 = P.n + 1;
+            const int64_t clo = lo <= 0 ? 0 : (lo + np1 - 1) / np1;
+            const int64_t chi = hi / np1;
+            pk_here = clo <= chi;
+        }
         const int64_t col0 = BATCHED ? (fm >> P.log2n) : fm / P.n;
         const int i0 = int(fm - col0 * P.n);
         const int c0 = int(col0);
@@ -272,7 +288,7 @@ __global__ __launch_bounds__(kThreads) void detect_flat_kernel(FlatParams P) {
             const int d = i - c;
             if (v[u].x != 0.0) { kl_t = max(kl_t, d); ku_t = max(ku_t, -d); }
             if (v[u].y != 0.0) { kl_t = max(kl_t, d + 1); ku_t = max(ku_t, -d - 1); }
-            if (PACK && f0 + e < P.total) {
+            if (pk_here && f0 + e < P.total) {
                 pack_store<PACK>(P.pk, mat, i, c, v[u].x);
                 pack_store<PACK>(P.pk, mat, i + 1, c, v[u].y);
             }
@@ -318,15 +334,19 @@ __global__ __launch_bounds__(256) void pack_fixup_kernel(Pack pk, int64_t n, int
                                                          const unsigned long long *klku) {
     if (klku[2] != 0ull) return;
     const int64_t kl = int64_t(klku[0]), ku = int64_t(klku[1]);
-    const int64_t rows = 2 * kl + ku + 1;
     const int64_t shift = pk.pkl + pk.pku - kl - ku;
-    const int64_t total = batch * n * rows;
-    for (int64_t g = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; g < total;
-         g += int64_t(gridDim.x) * blockDim.x) {
-        const int64_t r = g % rows, bc = g / rows;
+    const int lane = threadIdx.x & 63;
+    const int64_t wave = (int64_t(blockIdx.x) * blockDim.x + threadIdx.x) >> 6;
+    const int64_t waves = (int64_t(gridDim.x) * blockDim.x) >> 6;
+    // one wavefront per column: its fill rows 0..kl-1, and the rows of its
+    // slots above row 0 (c < ku) or below row n-1 (c > n-1-kl)
+    for (int64_t bc = wave; bc < batch * n; bc += waves) {
         const int64_t c = bc % n, b = bc / n;
-        const int64_t i = c + r - kl - ku;
-        if (r < kl || i < 0 || i >= n) pk.AB[b * pk.strideAB + shift + r + c * pk.ldab] = 0.0;
+        double *col = pk.AB + b * pk.strideAB + shift + c * pk.ldab;
+        const int64_t top = kl + (c < ku ? ku - c : 0);           // rows [0, top): fill or i < 0
+        const int64_t bot = kl + ku + (n - c);                     // rows [bot, 2kl+ku]: i >= n
+        for (int64_t r = lane; r < top; r += 64) col[r] = 0.0;
+        for (int64_t r = bot + lane; r <= 2 * kl + ku; r += 64) col[r] = 0.0;
     }
 }
 
@@ -466,7 +486,7 @@ int detect_convert(const double *dA, int64_t n, int64_t lda, int64_t strideA, in
         rc != BANDLU_OK)
         return rc;
     if (n == 0 || batch == 0) return BANDLU_OK;
-    const int64_t total = batch * n * (2 * kl_cap + ku_cap + 1);
+    const int64_t total = batch * n * 64;  // a wavefront per column
     const unsigned grid = (unsigned)std::min<int64_t>((total + 255) / 256, int64_t(device_cu_count()) * 16);
     hipLaunchKernelGGL(pack_fixup_kernel, dim3(grid), dim3(256), 0, s, pk, n, batch,
                        reinterpret_cast<const unsigned long long *>(batch == 1 && d_max == nullptr ? d_out : d_max));

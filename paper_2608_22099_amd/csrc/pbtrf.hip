@@ -40,7 +40,7 @@ struct CholParams {
 // LDS window: column c at slot c % (kd+2), entry r (row c+r) at slot*(kd+1)+r
 __global__ __launch_bounds__(kCholThreads) void pbtrf_lds_kernel(CholParams P) {
     extern __shared__ double win[];
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int n = P.n, kd = P.kd, W = kd + 2, H = kd + 1;
     double *AB = P.AB + int64_t(blockIdx.x) * P.strideAB;
     const int64_t ldab = P.ldab;
@@ -52,11 +52,25 @@ __global__ __launch_bounds__(kCholThreads) void pbtrf_lds_kernel(CholParams P) {
     }
     __syncthreads();
     int info = 0;
-    for (int j = 0; j < n; ++j) {
+    // the columns that enter are read kPf steps ahead (a register ring), so
+    // that no step waits for its load
+    constexpr int kPf = 4;
+    auto ld_enter = [&](int ce) -> double {
+        return (ce < n && tid < H && ce + tid < n) ? AB[tid + int64_t(ce) * ldab] : 0.0;
+    };
+    double ring[kPf];
+#pragma unroll
+    for (int q = 0; q < kPf; ++q) ring[q] = ld_enter(kd + 1 + q);
+    for (int j0 = 0; j0 < n && !info; j0 += kPf)
+#pragma unroll
+    for (int q = 0; q < kPf; ++q) {
+        const int j = j0 + q;
+        if (j >= n) break;
         const int kn = std::min(kd, n - 1 - j);
-        // the column that enters (j+kd+1), read from global before the update
+        // the column that enters (j+kd+1), loaded kPf steps ago
         const int ce = j + kd + 1;
-        const double enter = (ce < n && tid < H && ce + tid < n) ? AB[tid + int64_t(ce) * ldab] : 0.0;
+        const double enter = ring[q];
+        ring[q] = ld_enter(ce + kPf);
         const double d0 = at(j, 0);
         if (!(d0 > 0.0)) {
             info = j + 1;
@@ -64,16 +78,19 @@ __global__ __launch_bounds__(kCholThreads) void pbtrf_lds_kernel(CholParams P) {
         }
         const double d = __builtin_sqrt(d0);
         const double r = 1.0 / d;
-        // trailing update: pairs (a, b), 1 <= a <= b <= kn: A(j+b, j+a)
-        for (int q = tid; q < kn * kn; q += kCholThreads) {
-            const int a = q / kn + 1, b = q - (a - 1) * kn + 1;
-            if (b >= a) {
-                const double lb = at(j, b) * r, la = at(j, a) * r;
-                at(j + a, b - a) = __builtin_fma(-lb, la, at(j + a, b - a));
-            }
+        // trailing update A(j+b, j+a) for 1 <= a <= b <= kn: column j+a by
+        // wavefront, rows by lane (L(., j) formed where it is used)
+        const int sj = j % W;  // (one modulo per step; the other slots follow from it)
+        const double *cj = win + sj * H;
+        for (int a = 1 + wv; a <= kn; a += kCholThreads / 64) {
+            const int sa = sj + a >= W ? sj + a - W : sj + a;
+            double *ca = win + sa * H;
+            const double la = cj[a] * r;
+            for (int b = a + lane; b <= kn; b += 64)
+                ca[b - a] = __builtin_fma(-(cj[b] * r), la, ca[b - a]);
         }
         // column j is final
-        if (tid <= kn) AB[tid + int64_t(j) * ldab] = tid == 0 ? d : at(j, tid) * r;
+        if (tid <= kn) AB[tid + int64_t(j) * ldab] = tid == 0 ? d : cj[tid] * r;
         if (ce < n && tid < H) at(ce, tid) = enter;
         __syncthreads();
     }
@@ -105,12 +122,12 @@ __global__ __launch_bounds__(kCholThreads) void pbtrf_global_kernel(CholParams P
         }
         const double d = __builtin_sqrt(d0);
         const double r = 1.0 / d;
-        for (int64_t q = tid; q < int64_t(kn) * kn; q += kCholThreads) {
-            const int a = int(q / kn) + 1, b = int(q - int64_t(a - 1) * kn) + 1;
-            if (b >= a) {
-                const double lb = at(j, b) * r, la = at(j, a) * r;
-                at(j + a, b - a) = __builtin_fma(-lb, la, at(j + a, b - a));
-            }
+        // column j+a by wavefront, rows by lane
+        const int wvg = tid >> 6, lng = tid & 63;
+        for (int a = 1 + wvg; a <= kn; a += kCholThreads / 64) {
+            const double la = at(j, a) * r;
+            for (int b = a + lng; b <= kn; b += 64)
+                at(j + a, b - a) = __builtin_fma(-(at(j, b) * r), la, at(j + a, b - a));
         }
         __syncthreads();
         // column j is final (no later step reads it)
