@@ -5,10 +5,11 @@ matrix (or one batch) of synthetic dense-stored banded input already resident
 in HBM: band_detect (with the early-exit caps of the speedup constraint) ->
 one device-to-host copy of (kl, ku, exceeded) -> host policy (Sec. II-B
 speedup constraint) -> dense_to_band -> band_getrf -> band_getrs.  A single
-matrix takes the two halves of band_gbsv for the last two (the same results:
-"getrf" is the factorisation with the forward half of the solve, fused into
-the persistent wide-band launch where that kernel runs, "getrs" the backward
-half); a batch calls band_getrf_batched and band_getrs_batched.
+matrix that the persistent wide-band LU factors takes the two halves of
+band_gbsv for the last two (the same results: "getrf" is the factorisation
+with the forward half of the solve fused into that launch, "getrs" the
+backward half); other matrices and batches call band_getrf(_batched) and
+band_getrs(_batched).
 
 Prints ONE JSON line.  `value` is factorizations per second of the whole
 path; per-call times come from HIP events on the stream every call is enqueued
@@ -422,6 +423,8 @@ def main():
         det = torch.empty((batch, 3), dtype=torch.int64, device=dev)
         dmax = torch.empty(3, dtype=torch.int64, device=dev)
 
+    fused = batch == 1 and bandlu.band_getrf_variant(n, kl, ku, 1) == "wide"
+
     def step(timed):
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)] if timed else None
         if timed:
@@ -446,17 +449,22 @@ def main():
         x.copy_(b0)
         if timed:
             ev[3].record()
-        # one matrix: the factorisation with the forward half of the solve
-        # (fused into the persistent wide-band launch where that kernel runs),
-        # then the backward half -- band_getrf + band_getrs, the same results
-        if batch == 1:
+        # a matrix that the persistent wide-band LU factors: the factorisation
+        # with the forward half of the solve fused into it, then the backward
+        # half (band_getrf + band_getrs, the same results); otherwise the two
+        # calls themselves
+        if fused:
             bandlu.band_gbsv_lu(AB, kl_d, ku_d, x, ipiv=ipiv, info=info)
+        elif batch == 1:
+            bandlu.band_getrf(AB, kl_d, ku_d, ipiv=ipiv, info=info)
         else:
             bandlu.band_getrf_batched(AB, kl_d, ku_d, ipiv=ipiv, info=info)
         if timed:
             ev[4].record()
-        if batch == 1:
+        if fused:
             bandlu.band_gbsv_back(AB, kl_d, ku_d, x)
+        elif batch == 1:
+            bandlu.band_getrs(AB, kl_d, ku_d, ipiv, x)
         else:
             bandlu.band_getrs_batched(AB, kl_d, ku_d, ipiv, x)
         if timed:
@@ -503,7 +511,7 @@ def main():
         kernels[k]["algorithmic_bytes"] = costs[k]["bytes"]
     kernels["getrf"]["variant"] = variant
     kernels["getrs"]["variant"] = bandlu.band_getrs_variant(n, kl, ku, 1, batch)
-    if batch == 1:
+    if fused:
         kernels["getrf"]["entry"] = "band_gbsv_lu (factorisation + forward half of the solve)"
         kernels["getrs"]["entry"] = "band_gbsv_back (backward half of the solve)"
 
