@@ -18,11 +18,12 @@
 // When all panels before it are applied the block is itself the next panel:
 // its owner factors it in place (first with every pivot on the diagonal,
 // verified column by column against partial pivoting; on the first failure
-// again with partial pivoting), writes the factors to the band, and publishes
-// the panel's L (in the row order after the panel's interchanges, laid out for
-// the matrix-core operands) in a ring of G slots.  The owner of the next block
-// applies it at once, so the chain of panels never waits for a relaunch, and
-// the band is read from HBM once and written once.
+// again with partial pivoting), publishes the panel's L (in the row order
+// after the panel's interchanges, laid out for the matrix-core operands) in a
+// ring of G slots, and then writes the factors to the band (nothing on the
+// chain reads them there).  The owner of the next block applies the panel at
+// once, so the chain of panels never waits for a relaunch, and the band is
+// read from HBM once and written once.
 //
 // Every update of an entry is one fused multiply-add in the order of the
 // column steps (forward substitution and the matrix-core product both sum in
@@ -564,8 +565,9 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
         static_assert(NB == 32, "four groups of eight steps");
         // no interchange: pivots, multipliers and U stay in place.  Each row
         // goes back to its row of the window, and from there all threads
-        // write the panel's band entries and its published L with coalesced
-        // stores (one LDS read and one store per entry: few registers).
+        // write the panel's published L (before the hand-over) and its band
+        // entries (after it) with coalesced stores (one LDS read and one
+        // store per entry: few registers).
         // (Done in both branches below, so that the rows' registers are not
         // carried across their join.)
         auto commit_spec = [&]() __attribute__((always_inline)) {
@@ -580,9 +582,12 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
             }
         };
         // (after the barrier that follows commit_spec)
-        auto commit_stores = [&](unsigned zm) __attribute__((always_inline)) {
+        // the band entries of the panel's columns, column by column: no other
+        // workgroup reads them, so they are written after the hand-over (the
+        // release fence of the hand-over then waits for, and writes back, only
+        // the published L)
+        auto commit_band = [&]() __attribute__((always_inline)) {
             const int tt = opaque_v(t);
-            // the band entries of the panel's columns, column by column
 #pragma unroll 1
             for (int idx = tt; idx < NB * PR; idx += kThreads) {
                 const int c = idx / PR, w = idx - c * PR;
@@ -590,6 +595,9 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
                 if (c < nbn && w < Rn && d >= -kv && d <= kl)
                     AB[int64_t(j0 + c) * ldab + (kv + d)] = W[prow(j0 + w) * LDW + c];
             }
+        };
+        auto commit_slot = [&](unsigned zm) __attribute__((always_inline)) {
+            const int tt = opaque_v(t);
             // L11 (column-major) and -L21 (column-major); zero-pivot columns
             // and rows outside the matrix contribute nothing
 #pragma unroll 1
@@ -625,7 +633,7 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
         }
         if (spec_ok) {
             __syncthreads();
-            commit_stores(__builtin_amdgcn_readfirstlane(zmask));
+            commit_slot(__builtin_amdgcn_readfirstlane(zmask));
         } else {
             // ---- partial pivoting, in the window in LDS: one thread per row,
             // whole rows interchanged (so the window ends with L in its final
@@ -746,6 +754,10 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
         __syncthreads();
         if (t == 0) __hip_atomic_store(counter, b + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
         __syncthreads();
+        if (spec_ok) {
+            commit_band();
+            __syncthreads();  // the window is loaded again next
+        }
     }
 }
 
