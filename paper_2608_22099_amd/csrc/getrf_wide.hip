@@ -564,16 +564,29 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
         };
         static_assert(NB == 32, "four groups of eight steps");
         // no interchange: pivots, multipliers and U stay in place.  Each row
-        // goes back to its row of the window, and from there all threads
-        // write the panel's published L (before the hand-over) and its band
-        // entries (after it) with coalesced stores (one LDS read and one
-        // store per entry: few registers).
+        // writes its part of the published L from its registers, and goes
+        // back to its row of the window, from where all threads write the
+        // panel's band entries with coalesced stores after the hand-over (one
+        // LDS read and one store per entry: few registers).
         // (Done in both branches below, so that the rows' registers are not
         // carried across their join.)
         auto commit_spec = [&]() __attribute__((always_inline)) {
             if (myr >= 0) {
 #pragma unroll
                 for (int c = 0; c < NB; ++c) W[mp + c] = x[c];
+                // the published L straight from the registers, one store per
+                // column (consecutive rows: consecutive addresses): L11 for
+                // rows 0..31, -L21 below; zero-pivot columns, columns past
+                // the matrix and rows outside it contribute zeros
+                const unsigned zm = __builtin_amdgcn_readfirstlane(zmask);
+#pragma unroll
+                for (int sc = 0; sc < NB; ++sc) {
+                    const bool live = myr < Rn && sc < nbn && !((zm >> sc) & 1u);
+                    if (myr < NB)
+                        gL11[sc * NB + myr] = (live && sc < myr) ? x[sc] : 0.0;
+                    else
+                        gNL[sc * (PR - NB) + (myr - NB)] = live ? -x[sc] : 0.0;
+                }
             }
             if (t < nbn) ipiv[j0 + t] = j0 + t + 1;
             if (t == 0) {
@@ -596,21 +609,6 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
                     AB[int64_t(j0 + c) * ldab + (kv + d)] = W[prow(j0 + w) * LDW + c];
             }
         };
-        auto commit_slot = [&](unsigned zm) __attribute__((always_inline)) {
-            const int tt = opaque_v(t);
-            // L11 (column-major) and -L21 (column-major); zero-pivot columns
-            // and rows outside the matrix contribute nothing
-#pragma unroll 1
-            for (int idx = tt; idx < NB * PR; idx += kThreads) {
-                const int sc = idx / PR, w = idx - sc * PR;
-                const bool live = w < Rn && sc < nbn && !((zm >> sc) & 1u);
-                const double v = W[prow(j0 + w) * LDW + sc];
-                if (w < NB)
-                    gL11[sc * NB + w] = (live && sc < w) ? v : 0.0;
-                else
-                    gNL[sc * (PR - NB) + (w - NB)] = live ? -v : 0.0;
-            }
-        };
         bool spec_ok;
         if (__builtin_amdgcn_readfirstlane(wv) == 0) {
             group_w0.template operator()<0>();
@@ -631,10 +629,7 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
             spec_ok = s_viol == 0;
             if (spec_ok) commit_spec();
         }
-        if (spec_ok) {
-            __syncthreads();
-            commit_slot(__builtin_amdgcn_readfirstlane(zmask));
-        } else {
+        if (!spec_ok) {
             // ---- partial pivoting, in the window in LDS: one thread per row,
             // whole rows interchanged (so the window ends with L in its final
             // row order, as the blocks it updates need it), four barriers per
