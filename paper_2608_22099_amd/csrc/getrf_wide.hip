@@ -337,8 +337,14 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
                 const double2 *src = reinterpret_cast<const double2 *>(gNL);
                 double2 *dst = reinterpret_cast<double2 *>(sA);
                 constexpr int kPieces = (PR - NB) * NB / 2;
-#pragma unroll 4
-                for (int i = opaque_v(t - 64); i < kPieces; i += kThreads - 64) dst[i] = src[i];
+                // (every thread's 16 pieces in flight at once: one memory latency)
+                static_assert(kPieces % (kThreads - 64) == 0, "whole rounds");
+                const int i0 = opaque_v(t - 64);
+                double2 v[kPieces / (kThreads - 64)];
+#pragma unroll
+                for (int u = 0; u < kPieces / (kThreads - 64); ++u) v[u] = src[i0 + u * (kThreads - 64)];
+#pragma unroll
+                for (int u = 0; u < kPieces / (kThreads - 64); ++u) dst[i0 + u * (kThreads - 64)] = v[u];
             }
             if (wv == 0 && lane < NB) {
                 // rows j0..j0+31 are 32 consecutive physical rows (288 and
