@@ -578,12 +578,12 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
         // carried across their join.)
         auto commit_spec = [&]() __attribute__((always_inline)) {
             if (myr >= 0) {
-#pragma unroll
-                for (int c = 0; c < NB; ++c) W[mp + c] = x[c];
                 // the published L straight from the registers, one store per
                 // column (consecutive rows: consecutive addresses): L11 for
                 // rows 0..31, -L21 below; zero-pivot columns, columns past
-                // the matrix and rows outside it contribute zeros
+                // the matrix and rows outside it contribute zeros.  (Issued
+                // first: the hand-over waits for them; the copy to the window
+                // below goes on while they drain.)
                 const unsigned zm = __builtin_amdgcn_readfirstlane(zmask);
 #pragma unroll
                 for (int sc = 0; sc < NB; ++sc) {
@@ -593,6 +593,8 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
                     else
                         gNL[sc * (PR - NB) + (myr - NB)] = live ? -x[sc] : 0.0;
                 }
+#pragma unroll
+                for (int c = 0; c < NB; ++c) W[mp + c] = x[c];
             }
             if (t < nbn) ipiv[j0 + t] = j0 + t + 1;
             if (t == 0) {
