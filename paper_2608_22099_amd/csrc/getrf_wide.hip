@@ -478,15 +478,14 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
         // larger pivot key (a tie goes to the first, the diagonal), so every
         // row checks itself at every step instead of taking part in an argmax.
         // Wave 0 (rows 0..31, row s in lane s) runs the 32 steps, lane s
-        // publishing pivot row s in LDS; waves 1..4 apply each group of eight
-        // steps while wave 0 computes the next.  The operations are those of the pivoting loop
-        // below, so whenever it would not interchange, the results are its
-        // results.
+        // publishing pivot row s in LDS; waves 1..4 apply each group of steps
+        // while wave 0 computes the next.  The operations are those of the
+        // pivoting loop below, so whenever it would not interchange, the
+        // results are its results.
         bool viol = false;
         int finfo = 0;
         unsigned zmask = 0;  // columns whose pivot is zero
         if (t == 0) s_viol = 0;
-        const int ngrp = (nbn + 7) / 8;
         double r = 1.0 / x[0];  // wave 0: reciprocal of this row's entry in the next step's column
         double *const sUb = sU + opaque_v(0);  // (see the substitution above)
         // apply step S to a row held in xr (its window row wr, kept if !ok)
@@ -554,21 +553,23 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
                 if (finfo == 0) finfo = j0 + S + 1;
             }
         };
-        auto group_w0 = [&]<int Gp>() __attribute__((always_inline)) {
-            if (Gp >= ngrp) return;
+        // groups of steps S0..S0+CNT-1; the last groups are short, so that
+        // waves 1..4 (one group behind wave 0) finish soon after wave 0
+        auto group_w0 = [&]<int S0, int CNT>() __attribute__((always_inline)) {
+            if (S0 >= nbn) return;
             [&]<int... Q>(std::integer_sequence<int, Q...>) __attribute__((always_inline)) {
-                (step_w0.template operator()<8 * Gp + Q>(), ...);
-            }(std::make_integer_sequence<int, 8>{});
+                (step_w0.template operator()<S0 + Q>(), ...);
+            }(std::make_integer_sequence<int, CNT>{});
             lds_barrier();
         };
-        auto group_wk = [&]<int Gp>() __attribute__((always_inline)) {
-            if (Gp >= ngrp) return;
+        auto group_wk = [&]<int S0, int CNT>() __attribute__((always_inline)) {
+            if (S0 >= nbn) return;
             lds_barrier();
             [&]<int... Q>(std::integer_sequence<int, Q...>) __attribute__((always_inline)) {
-                (step_wk.template operator()<8 * Gp + Q>(), ...);
-            }(std::make_integer_sequence<int, 8>{});
+                (step_wk.template operator()<S0 + Q>(), ...);
+            }(std::make_integer_sequence<int, CNT>{});
         };
-        static_assert(NB == 32, "four groups of eight steps");
+        static_assert(NB == 32, "groups of 8, 8, 8, 4, 2 and 2 steps");
         // no interchange: pivots, multipliers and U stay in place.  Each row
         // writes its part of the published L from its registers, and goes
         // back to its row of the window, from where all threads write the
@@ -619,19 +620,23 @@ __global__ __launch_bounds__(kThreads) void getrf_wide_kernel(WideParams P) {
         };
         bool spec_ok;
         if (__builtin_amdgcn_readfirstlane(wv) == 0) {
-            group_w0.template operator()<0>();
-            group_w0.template operator()<1>();
-            group_w0.template operator()<2>();
-            group_w0.template operator()<3>();
+            group_w0.template operator()<0, 8>();
+            group_w0.template operator()<8, 8>();
+            group_w0.template operator()<16, 8>();
+            group_w0.template operator()<24, 4>();
+            group_w0.template operator()<28, 2>();
+            group_w0.template operator()<30, 2>();
             if (__ballot(viol) && lane == 0) s_viol = 1;
             lds_barrier();
             spec_ok = s_viol == 0;
             if (spec_ok) commit_spec();
         } else {
-            group_wk.template operator()<0>();
-            group_wk.template operator()<1>();
-            group_wk.template operator()<2>();
-            group_wk.template operator()<3>();
+            group_wk.template operator()<0, 8>();
+            group_wk.template operator()<8, 8>();
+            group_wk.template operator()<16, 8>();
+            group_wk.template operator()<24, 4>();
+            group_wk.template operator()<28, 2>();
+            group_wk.template operator()<30, 2>();
             if (__ballot(viol) && lane == 0) s_viol = 1;
             lds_barrier();
             spec_ok = s_viol == 0;
