@@ -183,6 +183,120 @@ __global__ __launch_bounds__(64) void lt_swap_kernel(LtParams P) {
     for (int q = lane; q < hi; q += 64) x[q] = ring[q & mask];
 }
 
+// The same pass for kl <= 1024 with both operands of every term in LDS: each
+// step's multipliers are staged next to the window (all lanes write their
+// prefetched part), the window keeps two copies of every position (at q mod R
+// and R + q mod R, so positions j+1 .. j+km are consecutive), and the chain of
+// fused multiply-adds reads two terms per LDS load, the same in every lane
+// (no lane reads, no copies to vector registers).  The sums are those of the
+// definition in its order, so the result is lt_swap_kernel's.
+constexpr int kLtDotMaxKl = 1024;
+
+// keeps the compiler from sinking the next block's LDS loads below this point
+__device__ __forceinline__ void lt_fence() { asm volatile("" ::: "memory"); }
+
+__global__ __launch_bounds__(64) void lt_dot_kernel(LtParams P) {
+    extern __shared__ double lds_lt[];
+    const int lane = threadIdx.x;
+    const int64_t sys = blockIdx.x;
+    const int64_t b = sys / P.nrhs, k = sys - b * P.nrhs;
+    const double *__restrict__ AB = P.AB + b * P.strideAB;
+    const int32_t *__restrict__ ipiv = P.ipiv + b * P.strideP;
+    double *x = P.B + b * P.strideB + k * P.ldb;
+    const int n = P.n, kl = P.kl, R = P.R, mask = R - 1;
+    double *const ring = lds_lt;           // 2R doubles
+    double *const lbuf = lds_lt + 2 * R;   // the step's multipliers, kl rounded up to 64
+    const int64_t ldab = P.ldab;
+    auto put = [&](int q, double v) {
+        ring[q & mask] = v;
+        ring[(q & mask) + R] = v;
+    };
+    int low = std::max(0, n - 64);  // lowest position loaded
+    int hi = n;                     // positions >= hi are stored back
+    if (low + lane < n) put(low + lane, x[low + lane]);
+    int ipv = 0, ipv_base = -1;
+    constexpr int kPre = 4;  // chunks of 64 multipliers prefetched a step ahead
+    const int nch = (kl + 63) / 64;
+    auto lcol = [&](int j, int ch) -> double {
+        const int km = std::min(kl, n - 1 - j);
+        const int t = 1 + 64 * ch + lane;
+        return (j >= 0 && t <= km) ? AB[P.kv + t + int64_t(j) * ldab] : 0.0;
+    };
+    double lnext[kPre];
+#pragma unroll
+    for (int ch = 0; ch < kPre; ++ch) lnext[ch] = lcol(n - 2, ch);
+    __syncthreads();
+    for (int j = n - 2; j >= 0; --j) {
+        if (j < low) {
+            const int nl = std::max(0, low - 64);
+            if (nl + lane < low) put(nl + lane, x[nl + lane]);
+            low = nl;
+        }
+        if (j < ipv_base || ipv_base < 0) {
+            ipv_base = std::max(0, j - 63);
+            ipv = ipv_base + lane <= j ? ipiv[ipv_base + lane] : 0;
+        }
+        const int km = std::min(kl, n - 1 - j);
+        // stage column j's multipliers (term t = 1 + u at lbuf[u]) and take
+        // column j-1's into the prefetch registers
+#pragma unroll
+        for (int ch = 0; ch < kPre; ++ch) {
+            if (ch < nch) lbuf[64 * ch + lane] = lnext[ch];
+            lnext[ch] = lcol(j - 1, ch);
+        }
+        for (int ch = kPre; ch < nch; ++ch) lbuf[64 * ch + lane] = lcol(j, ch);
+        __syncthreads();
+        const double *const w = ring + ((j + 1) & mask);
+        double acc = ring[j & mask];
+        const int nfull = km >> 6;
+        for (int ch = 0; ch < nfull; ++ch) {
+            const double *const lw = lbuf + 64 * ch;
+            const double *const xw = w + 64 * ch;
+            // blocks of 16 terms, the loads of the next block issued before
+            // the fused multiply-adds of this one (the LDS latency is then
+            // under the chain)
+            double la[2][16], xa[2][16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) {
+                la[0][u] = lw[u];
+                xa[0][u] = xw[u];
+            }
+#pragma unroll
+            for (int blk = 0; blk < 4; ++blk) {
+                if (blk + 1 < 4) {
+#pragma unroll
+                    for (int u = 0; u < 16; ++u) {
+                        la[(blk + 1) & 1][u] = lw[16 * (blk + 1) + u];
+                        xa[(blk + 1) & 1][u] = xw[16 * (blk + 1) + u];
+                    }
+                }
+                lt_fence();
+#pragma unroll
+                for (int u = 0; u < 16; ++u) acc = __builtin_fma(-la[blk & 1][u], xa[blk & 1][u], acc);
+            }
+        }
+        for (int u = 64 * nfull; u < km; ++u) acc = __builtin_fma(-lbuf[u], w[u], acc);
+        const int p = __builtin_amdgcn_readlane(ipv, j - ipv_base) - 1;
+        if (lane == 0) {
+            if (p != j && p > j && p < n) {
+                const double vp = ring[p & mask];
+                put(p, acc);
+                put(j, vp);
+            } else {
+                put(j, acc);
+            }
+        }
+        __syncthreads();
+        // positions >= j + kl are final: store a block of 64 once it is complete
+        if (hi - 64 >= j + kl && hi - 64 >= 0) {
+            x[hi - 64 + lane] = ring[(hi - 64 + lane) & mask];
+            hi -= 64;
+        }
+    }
+    __syncthreads();
+    for (int q = lane; q < hi; q += 64) x[q] = ring[q & mask];
+}
+
 __global__ void diag_div_kernel(const double *AB, int64_t ldab, int64_t strideAB, double *B,
                                 int64_t ldb, int64_t strideB, int64_t n, int64_t nrhs,
                                 int64_t total) {
@@ -348,8 +462,14 @@ int getrs_t(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *dAB, 
         return BANDLU_ERR_UNSUPPORTED;
     }
     T.R = R;
-    hipLaunchKernelGGL(lt_swap_kernel, dim3((unsigned)(batch * nrhs)), dim3(64),
-                       size_t(R) * sizeof(double), s, T);
+    if (kl <= kLtDotMaxKl) {
+        // two copies of the window and the step's multipliers (at most 40 KiB)
+        const size_t lds = (size_t(2) * R + size_t((kl + 63) / 64) * 64) * sizeof(double);
+        hipLaunchKernelGGL(lt_dot_kernel, dim3((unsigned)(batch * nrhs)), dim3(64), lds, s, T);
+    } else {
+        hipLaunchKernelGGL(lt_swap_kernel, dim3((unsigned)(batch * nrhs)), dim3(64),
+                           size_t(R) * sizeof(double), s, T);
+    }
     BANDLU_CHECK_LAUNCH("band_getrs_t (L^T pass)");
     return BANDLU_OK;
 }
