@@ -15,6 +15,15 @@
 // the whole batch, so each step is branch-free and a 16-step prefetch ring
 // stays in flight.  Every entry sees the same fused multiply-adds, in the same
 // order, as in the unblocked algorithm.
+//
+// A single wavefront per SIMD runs the chain of steps, one instruction at a
+// time, so the step's instruction count is its time.  Blocks of 16 steps away
+// from both ends of the matrix (every index in range, kl candidates at every
+// step) therefore take a lean step: no range tests, the load and store offsets
+// of step U read from two per-lane tables (the part that grows with j is one
+// scalar offset), and, when all four pivots are normal numbers, no zero-pivot
+// or small-pivot handling.  The pivots of a block are kept in a register and
+// stored once per block.
 #pragma once
 
 #include <cfloat>
@@ -26,10 +35,11 @@
 
 namespace bandlu {
 
-// value of lane K of this lane's row of 16
+// value of lane K of this lane's row of 16 (every lane is written, so the
+// old value is the source itself: no separate zeroing of the destination)
 template <int K>
 __device__ __forceinline__ int row_bcast_i(int v) {
-    return __builtin_amdgcn_update_dpp(0, v, 0x150 + K, 0xf, 0xf, false);
+    return __builtin_amdgcn_update_dpp(v, v, 0x150 + K, 0xf, 0xf, false);
 }
 
 template <int K>
@@ -49,6 +59,7 @@ __global__ __launch_bounds__(64) void getrf_g16_kernel(WinParams P) {
     const int gl = lane & 15;
     const int b = blockIdx.x * 4 + (lane >> 4);
     const bool live = b < P.batch;
+    const unsigned long long livemask = __builtin_amdgcn_ballot_w64(live);
     const int n = P.n, ku = P.ku, kv = kl + P.ku, ldab = int(P.ldab);
     // one buffer over the whole batch (the host checks that it is < 2 GiB)
     const Buf ab = make_buf(P.AB, uint32_t(int64_t(P.batch) * P.strideAB * 8));
@@ -63,6 +74,22 @@ __global__ __launch_bounds__(64) void getrf_g16_kernel(WinParams P) {
         const bool ok = c >= 0 && c < n && r >= 0 && r < n && unsigned(r - c + ku) <= unsigned(kv);
         return ok ? mbase + uint32_t(c * ldab + kv + r - c) * 8u : kOutside;
     };
+    // The lean steps' offsets: at step j = 16m + U, row j leaves to column
+    // co = j + d (d = ((gl + H - 1 - U) mod 16) - H + 1, stored while
+    // d <= kv) and row j + 16 + H is loaded for column c = j + e
+    // (e = 17 + ((gl - U - 1) mod 16), in the band while e <= ku + H + 16).
+    // Both offsets are a per-lane part that depends on U only plus the scalar
+    // (j - 16) * ldab * 8 (lean blocks have j >= 16, so that every per-lane
+    // part, 16 * ldab + d * (ldab-1) + kv with d >= -7, is positive).
+    uint32_t st_tab[16], ld_tab[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+        const int d = ((gl + H - 1 - u) & 15) - H + 1;
+        st_tab[u] = d <= kv ? mbase + uint32_t(16 * ldab + d * (ldab - 1) + kv) * 8u : kOutside;
+        const int e = 17 + ((gl - u - 1) & 15);
+        ld_tab[u] = e <= ku + H + 16 ? mbase + uint32_t(16 * ldab + e * (ldab - 1) + kv + 16 + H) * 8u
+                                     : kOutside;
+    }
 
     double a[16];
     double pf[PF];
@@ -71,27 +98,13 @@ __global__ __launch_bounds__(64) void getrf_g16_kernel(WinParams P) {
 #pragma unroll
     for (int k = 0; k < PF; ++k) pf[k] = buf_ld(ab, foff(k + H, colof(k + 1)));
     int ju = 0, info = 0;
+    int pv = 0;  // the 1-based pivot row of this block's step gl
 
-    auto step = [&]<int U>(int j) __attribute__((always_inline)) {
-        constexpr int S0 = U;  // slot of row j; lane U of each group holds column j
-        const int km = min(kl, n - 1 - j);
+    // steps 2..4 of the unblocked algorithm (interchange, multipliers,
+    // update) for any pivot
+    auto tail_any = [&]<int U>(int j, int p, double piv) __attribute__((always_inline)) {
+        constexpr int S0 = U;
         const int c = colof(j);
-        // ---- 1. pivot: the lane of column j scans its kl+1 rows (first
-        // largest |a|; a NaN counts only in first position), then its
-        // group takes the offset and the value from it
-        double best = a[S0], bk = __builtin_isnan(best) ? __builtin_inf() : fabs(best);
-        int pl = 0;
-#pragma unroll
-        for (int t = 1; t < H; ++t) {
-            const double v = a[(S0 + t) & 15];
-            const bool gt = t <= km && fabs(v) > bk;  // false for a NaN
-            bk = gt ? fabs(v) : bk;
-            best = gt ? v : best;
-            pl = gt ? t : pl;
-        }
-        const int p = row_bcast_i<U>(pl);
-        const double piv = row_bcast_d<U>(best);
-        buf_st_i32(pb, gl == U ? pbase + uint32_t(j) * 4u : kOutside, j + p + 1);
         const bool elim = piv != 0.0;
         info = (!elim && info == 0) ? j + 1 : info;
         if (elim) {
@@ -131,9 +144,68 @@ __global__ __launch_bounds__(64) void getrf_g16_kernel(WinParams P) {
                 }
             }
         }
+    };
+
+    auto step = [&]<int U, bool LEAN>(int j, uint32_t soff) __attribute__((always_inline)) {
+        constexpr int S0 = U;  // slot of row j; lane U of each group holds column j
+        const int km = LEAN ? kl : min(kl, n - 1 - j);
+        // ---- 1. pivot: the lane of column j scans its kl+1 rows (first
+        // largest |a|; a NaN counts only in first position: every comparison
+        // with it is false), then its group takes the offset and the value
+        double best = a[S0];
+        int pl = 0;
+#pragma unroll
+        for (int t = 1; t < H; ++t) {
+            const double v = a[(S0 + t) & 15];
+            const bool gt = (LEAN || t <= km) && fabs(v) > fabs(best);  // false for a NaN
+            best = gt ? v : best;
+            pl = gt ? t : pl;
+        }
+        const int p = row_bcast_i<U>(pl);
+        const double piv = row_bcast_d<U>(best);
+        pv = gl == U ? j + p + 1 : pv;
+        if constexpr (LEAN && H > 1) {
+            // all four pivots normal numbers: no zero-pivot step, no division
+            const bool normal = fabs(piv) >= DBL_MIN && fabs(piv) <= DBL_MAX;
+            if ((__builtin_amdgcn_ballot_w64(!normal) & livemask) == 0ull) {
+                const int c = j + ((gl - U) & 15);
+                ju = max(ju, j + ku + p);
+                const int pe = c <= ju ? p : 0;
+                double a0 = a[S0];
+#pragma unroll
+                for (int k = 1; k < H; ++k) {
+                    const bool hit = pe == k;
+                    const double ak = a[(S0 + k) & 15];
+                    a0 = hit ? ak : a0;
+                    a[(S0 + k) & 15] = hit ? a[S0] : ak;
+                }
+                a[S0] = a0;
+                if (gl == U) {
+                    const double rcp = 1.0 / piv;
+#pragma unroll
+                    for (int t = 1; t < H; ++t) a[(S0 + t) & 15] = a[(S0 + t) & 15] * rcp;
+                }
+                double lm[H];
+#pragma unroll
+                for (int t = 1; t < H; ++t) lm[t] = row_bcast_d<U>(a[(S0 + t) & 15]);
+                if (c > j && c <= ju) {
+                    const double uu = a[S0];
+#pragma unroll
+                    for (int t = 1; t < H; ++t) a[(S0 + t) & 15] = __builtin_fma(-lm[t], uu, a[(S0 + t) & 15]);
+                }
+            } else {
+                tail_any.template operator()<U>(j, p, piv);
+            }
+        } else {
+            tail_any.template operator()<U>(j, p, piv);
+        }
         // ---- 5. row j leaves (U row j for active columns, a multiplier for
         // retired ones); row j+H enters its slot from the prefetch ring
-        {
+        if constexpr (LEAN) {
+            buf_st_so(ab, st_tab[U], soff, a[S0]);
+            a[(S0 + H) & 15] = pf[U];
+            pf[U] = buf_ld_so(ab, ld_tab[U], soff);
+        } else {
             const int co = colof(j - H + 1);
             const bool ok = co < n && j >= co - kv;
             buf_st(ab, ok ? mbase + uint32_t(co * ldab + kv + j - co) * 8u : kOutside, a[S0]);
@@ -143,9 +215,19 @@ __global__ __launch_bounds__(64) void getrf_g16_kernel(WinParams P) {
     };
 
     for (int j0 = 0; j0 < n; j0 += PF) {
-        [&]<int... Us>(std::integer_sequence<int, Us...>) {
-            ((j0 + Us < n ? step.template operator()<Us>(j0 + Us) : (void)0), ...);
-        }(std::make_integer_sequence<int, PF>{});
+        // lean block: stores of columns >= 0 (j0 >= 16 > H - 1), loads of
+        // rows and columns < n, and kl candidates at every step
+        const bool lean = j0 >= PF && j0 + 2 * PF + kv + H < n;
+        if (lean) {
+            [&]<int... Us>(std::integer_sequence<int, Us...>) {
+                (step.template operator()<Us, true>(j0 + Us, uint32_t(j0 + Us - PF) * uint32_t(ldab) * 8u), ...);
+            }(std::make_integer_sequence<int, PF>{});
+        } else {
+            [&]<int... Us>(std::integer_sequence<int, Us...>) {
+                ((j0 + Us < n ? step.template operator()<Us, false>(j0 + Us, 0u) : (void)0), ...);
+            }(std::make_integer_sequence<int, PF>{});
+        }
+        buf_st_i32(pb, j0 + gl < n ? pbase + uint32_t(j0 + gl) * 4u : kOutside, pv);
     }
     if (live && gl == 0) P.info[b] = info;
 }
