@@ -310,14 +310,16 @@ __global__ __launch_bounds__(64) void getrs_win_kernel(RsParams P) {
 template <int K>
 __device__ __forceinline__ double rs_bcast(double v) {
     const long long x = __double_as_longlong(v);
-    const int lo = __builtin_amdgcn_update_dpp(0, (int)(x & 0xffffffffll), 0x150 + K, 0xf, 0xf, false);
-    const int hi = __builtin_amdgcn_update_dpp(0, (int)(x >> 32), 0x150 + K, 0xf, 0xf, false);
+    // (every lane is written: the old value is the source, no zeroing)
+    const int lo = __builtin_amdgcn_update_dpp((int)(x & 0xffffffffll), (int)(x & 0xffffffffll),
+                                               0x150 + K, 0xf, 0xf, false);
+    const int hi = __builtin_amdgcn_update_dpp((int)(x >> 32), (int)(x >> 32), 0x150 + K, 0xf, 0xf, false);
     return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
 }
 
 template <int K>
 __device__ __forceinline__ int rs_bcast_i(int v) {
-    return __builtin_amdgcn_update_dpp(0, v, 0x150 + K, 0xf, 0xf, false);
+    return __builtin_amdgcn_update_dpp(v, v, 0x150 + K, 0xf, 0xf, false);
 }
 
 // the 16-bit lane pattern `bits` (bit i = lane i of a group) in every group
@@ -325,12 +327,16 @@ __device__ __forceinline__ unsigned long long rs_groups(unsigned bits) {
     return 0x0001000100010001ull * (bits & 0xffffu);
 }
 
+// (kl is a template parameter: the interchange of the forward pass then
+// tests exactly kl candidate rows, with no test of kl per candidate)
+template <int KL>
 __global__ __launch_bounds__(64) void getrs_g16_kernel(RsParams P, int64_t systems) {
     const int lane = threadIdx.x, gl = lane & 15;
     const int64_t sys = int64_t(blockIdx.x) * 4 + (lane >> 4);
     const bool live = sys < systems;
     const int64_t bidx = live ? sys / P.nrhs : 0, k = live ? sys - bidx * P.nrhs : 0;
-    const int n = int(P.n), kl = int(P.kl), kv = int(P.kl + P.ku), ldab = int(P.ldab);
+    constexpr int kl = KL;
+    const int n = int(P.n), kv = int(P.kl + P.ku), ldab = int(P.ldab);
     const int64_t batch = (systems + P.nrhs - 1) / P.nrhs;
     const Buf ab = make_buf(P.AB, uint32_t(batch * P.strideAB * 8));
     const Buf pb = make_buf(P.ipiv, uint32_t(batch * P.strideP * 4));
@@ -341,7 +347,7 @@ __global__ __launch_bounds__(64) void getrs_g16_kernel(RsParams P, int64_t syste
     auto rowoff = [&](int r) -> uint32_t { return r >= 0 && r < n ? xbase + uint32_t(r) * 8u : kOutside; };
 
     // ------------------------------------------------------------ forward --
-    if (kl > 0 && n > 1) {
+    if (KL > 0 && n > 1) {
         double bv = buf_ld(xb, rowoff(gl));
         double nxt = buf_ld(xb, rowoff(16 + gl));
         int ipv = buf_ld_i32(pb, gl < n ? pbase + uint32_t(gl) * 4u : kOutside);
@@ -352,50 +358,62 @@ __global__ __launch_bounds__(64) void getrs_g16_kernel(RsParams P, int64_t syste
         };
 #pragma unroll
         for (int u = 0; u < 16; ++u) lr[u] = buf_ld(ab, loff(u, u));
+        // the multipliers' per-lane offsets for lean blocks (plus the scalar
+        // (j + 16) * ldab * 8)
+        uint32_t ltab[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) ltab[u] = abase + uint32_t(kv + ((gl - u) & 15)) * 8u;
+        // one step; LEAN: a block away from the end (kl rows below every
+        // step, every load in range), where the update masks are constants
+        auto fstep = [&]<int u, bool LEAN>(int j0, double &done) __attribute__((always_inline)) {
+            const int j = j0 + u;
+            if (!LEAN && j >= n - 1) return;
+            const int km = LEAN ? KL : min(kl, n - 1 - j);
+            const int toff = (gl - u) & 15;
+            const int d = rs_bcast_i<u>(ipv) - 1 - j;  // pivot offset of this group
+            if (__ballot(d != 0)) {
+                // exchange rows j and j+d (0 < d <= km) inside each group
+                const double bj0 = rs_bcast<u>(bv);
+                double bjn = bj0;
+                [&]<int... Ts>(std::integer_sequence<int, Ts...>) {
+                    (
+                        [&] {
+                            constexpr int t = Ts + 1;
+                            const double vt = rs_bcast<(u + t) & 15>(bv);
+                            bjn = d == t ? vt : bjn;
+                        }(),
+                        ...);
+                }(std::make_integer_sequence<int, KL>{});
+                const bool ok = d > 0 && d <= km;
+                bv = (ok && toff == 0) ? bjn : ((ok && toff == d) ? bj0 : bv);
+            }
+            const double bj = rs_bcast<u>(bv);
+            if (__builtin_amdgcn_inverse_ballot_w64(rs_groups(((1u << km) - 1) << (u + 1) |
+                                                              ((1u << km) - 1) >> (15 - u))))
+                bv = __builtin_fma(-lr[u], bj, bv);
+            if (__builtin_amdgcn_inverse_ballot_w64(rs_groups(1u << u))) {
+                done = bv;  // row j is final
+                bv = nxt;   // row j + 16 enters
+            }
+            if constexpr (LEAN)
+                lr[u] = buf_ld_so(ab, ltab[u], uint32_t(j + 16) * uint32_t(ldab) * 8u);
+            else
+                lr[u] = buf_ld(ab, loff(u, j + 16));
+        };
         for (int j0 = 0; j0 < n - 1; j0 += 16) {
             const int ipv_next =
                 buf_ld_i32(pb, j0 + 16 + gl < n ? pbase + uint32_t(j0 + 16 + gl) * 4u : kOutside);
             const double nxt_next = buf_ld(xb, rowoff(j0 + 32 + gl));
             double done = 0.0;
-            [&]<int... Us>(std::integer_sequence<int, Us...>) {
-                (
-                    [&] {
-                        constexpr int u = Us;
-                        const int j = j0 + u;
-                        if (j >= n - 1) return;
-                        const int km = min(kl, n - 1 - j);
-                        const int toff = (gl - u) & 15;
-                        const int d = rs_bcast_i<u>(ipv) - 1 - j;  // pivot offset of this group
-                        if (__ballot(d != 0)) {
-                            // exchange rows j and j+d (0 < d <= km) inside each group
-                            const double bj0 = rs_bcast<u>(bv);
-                            double bjn = bj0;
-                            [&]<int... Ts>(std::integer_sequence<int, Ts...>) {
-                                (
-                                    [&] {
-                                        constexpr int t = Ts + 1;
-                                        if (t <= kl) {
-                                            const double vt = rs_bcast<(u + t) & 15>(bv);
-                                            bjn = d == t ? vt : bjn;
-                                        }
-                                    }(),
-                                    ...);
-                            }(std::make_integer_sequence<int, 15>{});
-                            const bool ok = d > 0 && d <= km;
-                            bv = (ok && toff == 0) ? bjn : ((ok && toff == d) ? bj0 : bv);
-                        }
-                        const double bj = rs_bcast<u>(bv);
-                        if (__builtin_amdgcn_inverse_ballot_w64(rs_groups(((1u << km) - 1) << (u + 1) |
-                                                                          ((1u << km) - 1) >> (15 - u))))
-                            bv = __builtin_fma(-lr[u], bj, bv);
-                        if (__builtin_amdgcn_inverse_ballot_w64(rs_groups(1u << u))) {
-                            done = bv;  // row j is final
-                            bv = nxt;   // row j + 16 enters
-                        }
-                        lr[u] = buf_ld(ab, loff(u, j + 16));
-                    }(),
-                    ...);
-            }(std::make_integer_sequence<int, 16>{});
+            if (j0 + 32 + KL <= n) {
+                [&]<int... Us>(std::integer_sequence<int, Us...>) {
+                    (fstep.template operator()<Us, true>(j0, done), ...);
+                }(std::make_integer_sequence<int, 16>{});
+            } else {
+                [&]<int... Us>(std::integer_sequence<int, Us...>) {
+                    (fstep.template operator()<Us, false>(j0, done), ...);
+                }(std::make_integer_sequence<int, 16>{});
+            }
             buf_st(xb, j0 + gl < n - 1 ? rowoff(j0 + gl) : kOutside, done);
             ipv = ipv_next;
             nxt = nxt_next;
@@ -413,28 +431,45 @@ __global__ __launch_bounds__(64) void getrs_g16_kernel(RsParams P, int64_t syste
         };
 #pragma unroll
         for (int u = 0; u < 16; ++u) ur[u] = buf_ld(ab, uoff(u, n - 1 - u));
+        // the U entries' per-lane offsets for lean blocks (plus the scalar
+        // (j - 32) * ldab * 8; lean blocks have j >= 32, and every per-lane
+        // part is positive)
+        uint32_t utab[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) utab[u] = abase + uint32_t(16 * ldab + kv - ((gl - u) & 15)) * 8u;
+        // one step; LEAN: a block with kv rows above every step and every
+        // load in range (the update masks then do not change from block to
+        // block)
+        auto bstep = [&]<int u, bool LEAN>(int m0, double &done, double nxt) __attribute__((always_inline)) {
+            const int j = n - 1 - (m0 + u);
+            if (!LEAN && j < 0) return;
+            const double xj = rs_bcast<u>(bv / ur[u]);
+            const int tm = LEAN ? kv : min(kv, j);
+            if (__builtin_amdgcn_inverse_ballot_w64(rs_groups(((1u << tm) - 1) << (u + 1) |
+                                                              ((1u << tm) - 1) >> (15 - u))))
+                bv = __builtin_fma(-ur[u], xj, bv);
+            if (__builtin_amdgcn_inverse_ballot_w64(rs_groups(1u << u))) {
+                done = xj;  // row j is final
+                bv = nxt;   // row j - 16 enters
+            }
+            if constexpr (LEAN)
+                ur[u] = buf_ld_so(ab, utab[u], uint32_t(j - 32) * uint32_t(ldab) * 8u);
+            else
+                ur[u] = buf_ld(ab, uoff(u, j - 16));
+        };
         for (int m0 = 0; m0 < n; m0 += 16) {
             const double nxt = buf_ld(xb, rowoff(n - 1 - (m0 + 16 + gl)));
             double done = 0.0;
-            [&]<int... Us>(std::integer_sequence<int, Us...>) {
-                (
-                    [&] {
-                        constexpr int u = Us;
-                        const int j = n - 1 - (m0 + u);
-                        if (j < 0) return;
-                        const double xj = rs_bcast<u>(bv / ur[u]);
-                        const int tm = min(kv, j);
-                        if (__builtin_amdgcn_inverse_ballot_w64(rs_groups(((1u << tm) - 1) << (u + 1) |
-                                                                          ((1u << tm) - 1) >> (15 - u))))
-                            bv = __builtin_fma(-ur[u], xj, bv);
-                        if (__builtin_amdgcn_inverse_ballot_w64(rs_groups(1u << u))) {
-                            done = xj;  // row j is final
-                            bv = nxt;   // row j - 16 enters
-                        }
-                        ur[u] = buf_ld(ab, uoff(u, j - 16));
-                    }(),
-                    ...);
-            }(std::make_integer_sequence<int, 16>{});
+            // lean: every step of the block has j >= max(32, kv)
+            if (m0 + 48 + kv <= n) {
+                [&]<int... Us>(std::integer_sequence<int, Us...>) {
+                    (bstep.template operator()<Us, true>(m0, done, nxt), ...);
+                }(std::make_integer_sequence<int, 16>{});
+            } else {
+                [&]<int... Us>(std::integer_sequence<int, Us...>) {
+                    (bstep.template operator()<Us, false>(m0, done, nxt), ...);
+                }(std::make_integer_sequence<int, 16>{});
+            }
             buf_st(xb, rowoff(n - 1 - (m0 + gl)), done);
         }
     }
@@ -573,7 +608,14 @@ int launch_getrs(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double *
     }
     // many systems with a small band: sixteen lanes per system
     if (v == BANDLU_GETRS_G16) {
-        hipLaunchKernelGGL(getrs_g16_kernel, dim3((unsigned)((systems + 3) / 4)), dim3(64), 0, s, P,
+        using G16 = void (*)(RsParams, int64_t);
+        static constexpr G16 g16[16] = {
+            getrs_g16_kernel<0>,  getrs_g16_kernel<1>,  getrs_g16_kernel<2>,  getrs_g16_kernel<3>,
+            getrs_g16_kernel<4>,  getrs_g16_kernel<5>,  getrs_g16_kernel<6>,  getrs_g16_kernel<7>,
+            getrs_g16_kernel<8>,  getrs_g16_kernel<9>,  getrs_g16_kernel<10>, getrs_g16_kernel<11>,
+            getrs_g16_kernel<12>, getrs_g16_kernel<13>, getrs_g16_kernel<14>, getrs_g16_kernel<15>};
+        // (g16_fits: kl + ku <= 15)
+        hipLaunchKernelGGL(g16[kl], dim3((unsigned)((systems + 3) / 4)), dim3(64), 0, s, P,
                            systems);
         BANDLU_CHECK_LAUNCH("band_getrs (16 lanes per system)");
         return BANDLU_OK;
