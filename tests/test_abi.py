@@ -123,7 +123,7 @@ def test_argument_validation(lib):
 
 def test_variant_selection(lib):
     W, G16, GEN, BLK, MF, SP, DG, WD = 1, 2, 3, 4, 5, 6, 7, 8
-    assert lib.band_getrf_variant(1000, 3, 3, 1) == DG
+    assert lib.band_getrf_variant(1000, 3, 3, 1) == G16
     assert lib.band_getrf_variant(8192, 16, 16, 1) == DG
     assert lib.band_getrf_variant(300, 23, 17, 1) == DG
     assert lib.band_getrf_variant(300, 20, 22, 1) == SP
@@ -131,7 +131,8 @@ def test_variant_selection(lib):
     assert lib.band_getrf_variant(300, 15, 24, 1) == SP
     assert lib.band_getrf_variant(300, 1, 24, 1) == DG
     assert lib.band_getrf_variant(300, 2, 25, 1) == SP
-    assert lib.band_getrf_variant(256, 4, 4, 63) == DG
+    assert lib.band_getrf_variant(256, 4, 4, 63) == G16
+    assert lib.band_getrf_variant(256, 5, 4, 63) == DG
     assert lib.band_getrf_variant(16384, 2, 64, 1) == SP
     assert lib.band_getrf_variant(300, 15, 97, 1) == SP
     assert lib.band_getrf_variant(300, 0, 5, 1) == W

@@ -254,10 +254,16 @@ def check_exact(T, kl, ku, what, variant=None):
 
 @pytest.mark.parametrize("n,kl,ku", DIAG_SHAPES)
 def test_getrf_diag_exact(n, kl, ku):
-    assert bandlu.band_getrf_variant(n, kl, ku) == "diag"
-    g, o = check_exact(dominant_band(n, kl, ku, 77 + n + ku), kl, ku, f"dominant n={n} kl={kl} ku={ku}")
+    # (the default for 1 <= kl <= 4, 2kl+ku+1 <= 16 is WINDOW_G16: the
+    # diagonal-pivot kernel is forced here, and the default checked too)
+    assert bandlu.band_getrf_variant(n, kl, ku) == (
+        "window_g16" if 1 <= kl <= 4 and 2 * kl + ku + 1 <= 16 else "diag")
+    g, o = check_exact(dominant_band(n, kl, ku, 77 + n + ku), kl, ku, f"dominant n={n} kl={kl} ku={ku}",
+                       variant="diag")
     assert np.array_equal(o[2], np.arange(1, n + 1))
-    check_exact(random_band(n, kl, ku, 78 + n + ku), kl, ku, f"random n={n} kl={kl} ku={ku}")
+    check_exact(random_band(n, kl, ku, 78 + n + ku), kl, ku, f"random n={n} kl={kl} ku={ku}",
+                variant="diag")
+    check_exact(random_band(n, kl, ku, 79 + n + ku), kl, ku, f"default kernel n={n} kl={kl} ku={ku}")
 
 
 @pytest.mark.parametrize("n,kl,ku,cols", [(300, 16, 16, (0, 1, 2, 3, 17, 18, 19, 35, 36, 37, 53, 54, 100, 298, 299)),
@@ -332,8 +338,8 @@ def test_getrf_diag_extreme_magnitudes():
     divide instead), through the diagonal-pivot kernel, bitwise."""
     for n, kl, ku in ((400, 16, 16), (300, 3, 3), (250, 7, 24)):
         T = dominant_band(n, kl, ku, 4242 + ku) * _column_scales(n)[:, None]  # row j of T is column j of A
-        assert bandlu.band_getrf_variant(n, kl, ku) == "diag"
-        check_exact(T, kl, ku, f"scaled columns n={n} kl={kl} ku={ku}")
+        check_exact(T, kl, ku, f"scaled columns n={n} kl={kl} ku={ku}", variant="diag")
+        check_exact(T, kl, ku, f"scaled columns, default kernel n={n} kl={kl} ku={ku}")
 
 
 def test_getrf_diag_fill_rows_not_read():
