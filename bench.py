@@ -43,17 +43,25 @@ METRIC = "band-LU factorizations/s + detect GB/s (fraction of HBM/FP64 peak), 1 
 STEPS = ["detect", "convert", "getrf", "getrs"]
 
 
-def kernel_costs(n, kl, ku, batch):
-    """Algorithmic bytes / flops per call of each step."""
+def kernel_costs(n, kl, ku, batch, fused=False):
+    """Algorithmic bytes / flops per call of each step.  fused: the getrf step
+    also runs the forward half of the solve (its multipliers, interchanges
+    and right-hand side), and the getrs step is the backward half alone (U
+    and the right-hand side)."""
     ldab = 2 * kl + ku + 1
     inband = sum(min(n - 1, j + kl) - max(0, j - ku) + 1 for j in range(n))
-    return {
+    costs = {
         "detect": {"bytes": 8.0 * n * n * batch},
         "convert": {"bytes": 8.0 * (inband + ldab * n) * batch},
         "getrf": {"bytes": (8.0 * (kl + ku + 1) * n + 8.0 * ldab * n + 4.0 * n) * batch,
                   "flops": 2.0 * n * kl * (kl + ku + 1) * batch},
         "getrs": {"bytes": (8.0 * ldab * n + 4.0 * n + 16.0 * n) * batch},
     }
+    if fused:
+        costs["getrf"]["bytes"] += (8.0 * kl * n + 4.0 * n + 16.0 * n) * batch
+        costs["getrf"]["flops"] += 2.0 * n * kl * batch
+        costs["getrs"]["bytes"] = (8.0 * (kl + ku + 1) * n + 16.0 * n) * batch
+    return costs
 
 
 # HIP sources each step's kernels are built from
@@ -491,7 +499,7 @@ def main():
     value = batch * 1e3 / ms_per_step  # factorizations per second, whole path
     timed_out = (AB.cpu().numpy(), ipiv.cpu().numpy(), info.cpu().numpy(), x.cpu().numpy())
 
-    costs = kernel_costs(n, kl, ku, batch)
+    costs = kernel_costs(n, kl, ku, batch, fused)
     kernels = {k: roofline_entry(k, avg[k], costs[k]) for k in STEPS}
     dom = max(STEPS, key=lambda k: avg[k])
     d = kernels[dom]
