@@ -68,7 +68,8 @@ def kernel_costs(n, kl, ku, batch, fused=False):
 STEP_SOURCES = {
     "detect": ["detect.hip", "common.hpp"],
     "convert": ["convert.hip", "common.hpp"],
-    "getrf": ["getrf.hip", "getrf_win64.hpp", "getrf_win2.hpp", "getrf_window.hpp", "getrf_g16.hpp",
+    "getrf": ["getrf.hip", "getrf_win64.hpp", "getrf_win2.hpp", "getrf_lean64.hpp", "getrf_window.hpp",
+              "getrf_g16.hpp",
               "getrf_split.hpp", "getrf_diag.hpp", "getrf_blocked.hip", "getrf_mfma.hip",
               "getrf_wide.hip", "chain.hip", "wave.hpp", "bufio.hpp", "common.hpp"],
     "getrs": ["getrs.hip", "getrs_ring.hpp", "getrs_ring.hip", "getrs_lane.hip", "chain.hip",

@@ -220,6 +220,11 @@ __global__ void zero_info_kernel(int32_t *info, int64_t batch) {
     if (i < batch) info[i] = 0;
 }
 
+// Up to this kl the one-wavefront window kernel with wave-uniform pivots
+// (getrf_lean64.hpp) takes fewer cycles per column than the two-wavefront
+// kernel, for single matrices and after a failed diagonal-pivot check.
+constexpr int64_t kLeanMaxKl = 6;
+
 int select_variant(int64_t n, int64_t kl, int64_t ku, int64_t batch) {
     const int64_t need = 2 * kl + ku + 1;
     if (batch >= 64 && kl <= 7 && need <= 32) return BANDLU_GETRF_WINDOW_G16;
@@ -228,6 +233,8 @@ int select_variant(int64_t n, int64_t kl, int64_t ku, int64_t batch) {
     // is within about 10 % of DIAG when none are and 2x faster when they are
     if (kl >= 1 && kl <= 4 && need <= 16) return BANDLU_GETRF_WINDOW_G16;
     if (diag_fits(n, kl, ku, need)) return BANDLU_GETRF_DIAG;
+    if (kl >= 1 && kl <= kLeanMaxKl && need <= 128 && need * n * 8 <= kMaxBufferBytes)
+        return BANDLU_GETRF_WINDOW;
     if (kl >= 1 && kl <= 31 && (need <= 64 || (need <= 128 && kl <= 15)) &&
         need * n * 8 <= kMaxBufferBytes)
         return BANDLU_GETRF_SPLIT;
@@ -379,7 +386,9 @@ int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
         W.kl = (int)kl;
         W.resume = 0;
         const WinKernel k = diag_kernel((int)ku);
-        const WinKernel rest = split_kernel(1, (int)kl + 1);
+        // (the band fits 64 lanes: 2kl+ku+1 <= 64)
+        const bool lean = kl <= kLeanMaxKl;
+        const WinKernel rest = lean ? win_kernel(64, 1, (int)kl + 1) : split_kernel(1, (int)kl + 1);
         if (!k || !rest) {
             set_error("band_getrf: no diagonal-pivot kernel for kl = %lld, ku = %lld", (long long)kl,
                       (long long)ku);
@@ -390,8 +399,8 @@ int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
         // columns from the first failing one on (a launch that returns at
         // once where every column passed)
         W.resume = 1;
-        hipLaunchKernelGGL(rest, dim3((unsigned)batch), dim3(128), 0, s, W);
-        BANDLU_CHECK_LAUNCH("band_getrf (two wavefronts, resumed)");
+        hipLaunchKernelGGL(rest, dim3((unsigned)batch), dim3(lean ? 64 : 128), 0, s, W);
+        BANDLU_CHECK_LAUNCH("band_getrf (diagonal pivots, resumed)");
         return BANDLU_OK;
     }
     if (v == BANDLU_GETRF_BLOCKED)

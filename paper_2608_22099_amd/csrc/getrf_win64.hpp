@@ -37,6 +37,7 @@
 #include "common.hpp"
 #include "getrf_window.hpp"
 #include "getrf_win2.hpp"
+#include "getrf_lean64.hpp"
 
 namespace bandlu {
 
@@ -293,12 +294,13 @@ __global__ __launch_bounds__(64) void getrf_win64_kernel(WinParams P) {
     if (L == 0) P.info[b] = info;
 }
 
-// One column per lane with a transposed pivot column from H = 7 on
-// (getrf_win2.hpp); the in-lane pivot scan below that and for two columns per
-// lane.
+// kl <= 7: the wave-uniform pivot kernel (getrf_lean64.hpp); beyond, one
+// column per lane with a transposed pivot column (getrf_win2.hpp), and the
+// in-lane pivot scan for two columns per lane.
 template <int H, int CPL>
 constexpr WinKernel win64_pick() {
-    if constexpr (CPL == 1 && H >= 7) return &getrf_win2_kernel<H, win_pf(H)>;
+    if constexpr (H <= 8) return &getrf_lean64_kernel<H, CPL>;
+    else if constexpr (CPL == 1) return &getrf_win2_kernel<H, win_pf(H)>;
     else return &getrf_win64_kernel<H, CPL, win_pf(H)>;
 }
 

@@ -39,7 +39,7 @@ struct WinParams {
     int64_t ldab, strideAB, strideP;
     int n, ku, batch;
     int kl;      // read by the kernels that take kl at run time
-    int resume;  // two-wavefront kernel: continue where the diagonal-pivot kernel stopped
+    int resume;  // two-wavefront and lean window kernels: continue where the diagonal-pivot kernel stopped
 };
 
 template <int G>

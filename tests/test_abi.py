@@ -130,10 +130,15 @@ def test_variant_selection(lib):
     assert lib.band_getrf_variant(300, 3, 24, 1) == DG
     assert lib.band_getrf_variant(300, 15, 24, 1) == SP
     assert lib.band_getrf_variant(300, 1, 24, 1) == DG
-    assert lib.band_getrf_variant(300, 2, 25, 1) == SP
+    # kl <= 6 beyond the diagonal-pivot kernel's reach: the lean window
+    assert lib.band_getrf_variant(300, 2, 25, 1) == W
+    assert lib.band_getrf_variant(300, 6, 40, 1) == W
+    assert lib.band_getrf_variant(300, 6, 115, 1) == W
+    assert lib.band_getrf_variant(300, 6, 116, 1) == BLK
+    assert lib.band_getrf_variant(300, 7, 40, 1) == SP
     assert lib.band_getrf_variant(256, 4, 4, 63) == G16
     assert lib.band_getrf_variant(256, 5, 4, 63) == DG
-    assert lib.band_getrf_variant(16384, 2, 64, 1) == SP
+    assert lib.band_getrf_variant(16384, 2, 64, 1) == W
     assert lib.band_getrf_variant(300, 15, 97, 1) == SP
     assert lib.band_getrf_variant(300, 0, 5, 1) == W
     assert lib.band_getrf_variant(300, 16, 97, 1) == BLK

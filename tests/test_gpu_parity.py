@@ -230,6 +230,41 @@ def test_getrf_split_special():
         assert_bitwise(g[1], o[1], what)
 
 
+# The one-wavefront window for kl <= 7 decides each pivot on scalars and runs
+# blocks of 16 steps away from both ends without range tests: long bands that
+# cross many 64-column periods (two columns per lane from 2kl+ku+1 = 65 on),
+# lengths off the block size, and both widths at their limits.
+LEAN_SHAPES = [(600, 0, 5), (601, 1, 1), (555, 2, 64), (700, 3, 3), (640, 4, 40), (603, 5, 100),
+               (650, 6, 50), (700, 7, 20), (700, 7, 113), (700, 1, 61), (700, 1, 62), (97, 7, 6)]
+
+
+@pytest.mark.parametrize("n,kl,ku", LEAN_SHAPES)
+def test_getrf_window_lean_exact(n, kl, ku):
+    for shift in (0.0, float(kl + ku)):
+        T = random_band(n, kl, ku, 7 + n + 10 * kl + ku, shift=shift)
+        check_exact(T, kl, ku, f"window n={n} kl={kl} ku={ku} shift={shift}", variant="window")
+
+
+@pytest.mark.parametrize("kl,ku", [(3, 10), (2, 64), (7, 113)])
+def test_getrf_window_lean_special(kl, ku):
+    """Zero pivots, NaN and Inf entries, -0.0, and a column of subnormal
+    numbers (its pivot is below DBL_MIN: the entries are divided) in the
+    middle of the band, where the blocks take the lean steps."""
+    n = 640
+    T = random_band(n, kl, ku, 1234 + kl)
+    T[:, 300] = 0.0                        # singular: info = 301 unless an earlier one
+    T[:, 200] = 0.0
+    T[320, max(0, 320 - min(kl, 1))] = np.nan
+    T[400, 400 + min(ku, 1)] = np.inf
+    T[450 - min(ku, 2): 451 + kl, 450] *= 1e-310   # subnormal column
+    T[500, 500] = -0.0
+    T[501, 501 + min(ku, 3)] = -0.0
+    check_exact(T, kl, ku, f"special kl={kl} ku={ku}", variant="window")
+    # a zero matrix and a matrix whose only nonzeros are tiny
+    check_exact(np.zeros((n, n)), kl, ku, "zero", variant="window")
+    check_exact(random_band(n, kl, ku, 99) * 1e-305, kl, ku, "tiny", variant="window")
+
+
 # The diagonal-pivot kernel must give the oracle's factors bit for bit
 # whether every column keeps its diagonal pivot (dominant bands), a column
 # fails the check (the two-wavefront kernel takes over there) or the first
