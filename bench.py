@@ -5,11 +5,11 @@ matrix (or one batch) of synthetic dense-stored banded input already resident
 in HBM: band_detect (with the early-exit caps of the speedup constraint) ->
 one device-to-host copy of (kl, ku, exceeded) -> host policy (Sec. II-B
 speedup constraint) -> dense_to_band -> band_getrf -> band_getrs.  A single
-matrix that the persistent wide-band LU factors takes the two halves of
-band_gbsv for the last two (the same results: "getrf" is the factorisation
-with the forward half of the solve fused into that launch, "getrs" the
-backward half); other matrices and batches call band_getrf(_batched) and
-band_getrs(_batched).
+matrix that the persistent wide-band LU or the lean window LU (1 <= kl <= 6)
+factors takes the two halves of band_gbsv for the last two (the same
+results: "getrf" is the factorisation with the forward half of the solve
+fused into that launch, "getrs" the backward half); other matrices and
+batches call band_getrf(_batched) and band_getrs(_batched).
 
 Prints ONE JSON line.  `value` is factorizations per second of the whole
 path; per-call times come from HIP events on the stream every call is enqueued
@@ -76,7 +76,7 @@ STEP_SOURCES = {
               "bufio.hpp", "common.hpp"],
 }
 # instantiation files of a step (one per parameter range), by name prefix
-STEP_PREFIXES = {"getrf": ("getrf_win_g", "getrf_split_c", "getrf_diag_ku"),
+STEP_PREFIXES = {"getrf": ("getrf_win_g", "getrf_lean_fwd", "getrf_split_c", "getrf_diag_ku"),
                  "getrs": ("getrs_ring_fwd", "getrs_ring_bwd", "getrs_ring_div")}
 
 
@@ -432,7 +432,11 @@ def main():
         det = torch.empty((batch, 3), dtype=torch.int64, device=dev)
         dmax = torch.empty(3, dtype=torch.int64, device=dev)
 
-    fused = batch == 1 and bandlu.band_getrf_variant(n, kl, ku, 1) == "wide"
+    # the kernels that run the forward solve inside the factorisation
+    # (band_gbsv_lu): the persistent wide-band LU, and the lean window LU
+    # (the window variant for 1 <= kl <= 6) with one right-hand side
+    variant1 = bandlu.band_getrf_variant(n, kl, ku, 1)
+    fused = batch == 1 and (variant1 == "wide" or (variant1 == "window" and 1 <= kl <= 6))
 
     def step(timed):
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)] if timed else None
@@ -458,10 +462,10 @@ def main():
         x.copy_(b0)
         if timed:
             ev[3].record()
-        # a matrix that the persistent wide-band LU factors: the factorisation
-        # with the forward half of the solve fused into it, then the backward
-        # half (band_getrf + band_getrs, the same results); otherwise the two
-        # calls themselves
+        # a matrix that the persistent wide-band LU or the lean window LU
+        # factors: the factorisation with the forward half of the solve fused
+        # into it, then the backward half (band_getrf + band_getrs, the same
+        # results); otherwise the two calls themselves
         if fused:
             bandlu.band_gbsv_lu(AB, kl_d, ku_d, x, ipiv=ipiv, info=info)
         elif batch == 1:

@@ -31,6 +31,8 @@ int launch_getrf_wide(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ld
                       int64_t batch, hipStream_t s, void *scratch, size_t scratch_bytes,
                       double *dB, int64_t ldb, int64_t strideB, int64_t nrhs);
 bool getrf_wide_fused_fits(int64_t n, int64_t kl, int64_t ku, int64_t nrhs);
+int launch_getrf_lean_fwd(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
+                          int32_t *d_ipiv, double *dB, int32_t *d_info, hipStream_t s);
 
 namespace {
 
@@ -583,8 +585,10 @@ extern "C" int band_getrs_t_batched(int64_t n, int64_t kl, int64_t ku, int64_t n
 // Factor and solve (xGBSV) as two calls with one dominant kernel each:
 //   band_gbsv_lu:   band_getrf, and L y = P b on the right-hand sides (inside
 //                   the persistent wide-band launch when that kernel runs, in
-//                   a workgroup that trails the chain of panels; else the
-//                   forward chain after the factorisation);
+//                   a workgroup that trails the chain of panels; inside the
+//                   lean window kernel's steps for one right-hand side when
+//                   that kernel runs; else the forward chain after the
+//                   factorisation);
 //   band_gbsv_back: U x = y, the backward chain.
 // band_gbsv is the two in turn.  The results are those of band_getrf and
 // band_getrs, bitwise.
@@ -624,6 +628,12 @@ extern "C" int band_gbsv_lu(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, dou
         getrf_wide_fused_fits(n, kl, ku, nrhs))
         return launch_getrf_wide(n, kl, ku, dAB, ldab, ldab * n, d_ipiv, n, d_info, 1, s, nullptr,
                                  0, dB, ldb, ldb * nrhs, nrhs);
+    // one right-hand side and the lean window kernel: the forward solve runs
+    // in the factorisation's own steps
+    if (nrhs == 1) {
+        const int rc = launch_getrf_lean_fwd(n, kl, ku, dAB, ldab, d_ipiv, dB, d_info, s);
+        if (rc != BANDLU_ERR_UNSUPPORTED) return rc;
+    }
     if (int rc = band_getrf(n, kl, ku, dAB, ldab, d_ipiv, d_info, stream); rc != BANDLU_OK)
         return rc;
     if (n < 2 || nrhs == 0 || kl == 0) return BANDLU_OK;

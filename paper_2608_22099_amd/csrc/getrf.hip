@@ -54,6 +54,9 @@ WinKernel split_kernel_c1_h17_32(int H);
 WinKernel split_kernel_c2_h2_16(int H);
 
 // two-wavefront kernel (getrf_split.hpp) for 2 <= H <= 32
+WinKernel lean64_fwd_kernel_c1(int H);
+WinKernel lean64_fwd_kernel_c2(int H);
+
 WinKernel split_kernel(int CPL, int H) {
     if (CPL == 1) return H <= 16 ? split_kernel_c1_h2_16(H) : split_kernel_c1_h17_32(H);
     return split_kernel_c2_h2_16(H);
@@ -428,6 +431,38 @@ int launch_getrf(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
 }
 
 }  // namespace
+
+// band_gbsv_lu for one right-hand side where the lean window kernel is the
+// one band_getrf runs: the factorisation and the forward solve in one launch.
+// Returns BANDLU_ERR_UNSUPPORTED (having launched nothing) where it is not.
+int launch_getrf_lean_fwd(int64_t n, int64_t kl, int64_t ku, double *dAB, int64_t ldab,
+                          int32_t *d_ipiv, double *dB, int32_t *d_info, hipStream_t s) {
+    const int64_t need = 2 * kl + ku + 1;
+    if (n < 1 || kl < 1 || kl > kLeanMaxKl || select_variant(n, kl, ku, 1) != BANDLU_GETRF_WINDOW ||
+        !variant_fits(BANDLU_GETRF_WINDOW, n, kl, ku, ldab, 1) || n * 8 > kMaxBufferBytes)
+        return BANDLU_ERR_UNSUPPORTED;
+    const int H = (int)kl + 1;
+    const WinKernel k = need <= 64 ? lean64_fwd_kernel_c1(H) : lean64_fwd_kernel_c2(H);
+    if (!k) return BANDLU_ERR_UNSUPPORTED;
+    WinParams W;
+    W.AB = dAB;
+    W.ipiv = d_ipiv;
+    W.info = d_info;
+    W.ldab = ldab;
+    W.strideAB = ldab * n;
+    W.strideP = n;
+    W.n = (int)n;
+    W.ku = (int)ku;
+    W.batch = 1;
+    W.kl = (int)kl;
+    W.resume = 0;
+    W.B = dB;
+    W.strideB = n;
+    hipLaunchKernelGGL(k, dim3(1), dim3(64), 0, s, W);
+    BANDLU_CHECK_LAUNCH("band_gbsv_lu (lean window with the forward solve)");
+    return BANDLU_OK;
+}
+
 }  // namespace bandlu
 
 using namespace bandlu;

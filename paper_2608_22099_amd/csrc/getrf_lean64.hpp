@@ -22,7 +22,16 @@
 //      active columns, a multiplier for retired ones) and refills the slot of
 //      row j+kl+1 from a prefetch ring 16 steps deep.
 // The operations and their order are those of the unblocked algorithm, so
-// the factors are bitwise equal to it.  Blocks of 16 steps away from both
+// the factors are bitwise equal to it.
+//
+// FWD: the forward half of the solve (xGBTRS's L y = P b, one right-hand side)
+// runs in the same steps: rows j..j+kl of b are wave-uniform values in a
+// 16-slot ring; step j interchanges rows j and j+p, keeps y(j), and step j+1
+// applies step j's
+//   b(j+t) = fma(-l(j+t,j), y(j), b(j+t)),  t = 1..kl,
+// with the multipliers as stored (the raw column for a zero pivot), as the
+// plain forward loop does.  Rows enter from two registers that hold a block
+// of 16 rows each in lanes 0..15; y leaves one block at a time.  Blocks of 16 steps away from both
 // ends (every index in range, kl candidates at every step) address memory
 // with a per-lane offset plus one scalar offset and test no ranges; the
 // blocks at the ends check every index.
@@ -48,7 +57,7 @@ __device__ __forceinline__ double own_copy(double x) {
     return y;
 }
 
-template <int H, int CPL>
+template <int H, int CPL, bool FWD = false>
 __global__ __launch_bounds__(64) void getrf_lean64_kernel(WinParams P) {
     static_assert(H >= 1 && H <= 8, "kl <= 7");
     static_assert(CPL == 1 || CPL == 2, "one or two columns per lane");
@@ -105,6 +114,20 @@ __global__ __launch_bounds__(64) void getrf_lean64_kernel(WinParams P) {
     }
     int ju = 0, info = 0;
     int pv = 0;  // lane U < 16: the 1-based pivot row of this block's step U
+
+    // forward solve: rows of b by slot r mod 16, the block's rows and the
+    // next block's in lanes 0..15, y(j) of step U in lane U
+    const Buf bb = make_buf(FWD ? P.B + b * P.strideB : P.AB, FWD ? uint32_t(n) * 8u : 0u);
+    double bw[16], bcur = 0.0, bnext = 0.0, yv = 0.0;
+    double lp[H], yp = 0.0;  // the last step's multipliers (as stored) and y
+#pragma unroll
+    for (int t = 0; t < H; ++t) lp[t] = 0.0;
+    if constexpr (FWD) {
+        bcur = buf_ld(bb, L < PF ? uint32_t(L) * 8u : kOutside);
+        bnext = buf_ld(bb, L < PF ? uint32_t(PF + L) * 8u : kOutside);
+#pragma unroll
+        for (int r = 0; r < H; ++r) bw[r] = own_copy(readlane_d(bcur, r));
+    }
 
     auto step = [&]<int U, bool LEAN>(int j) __attribute__((always_inline)) {
         constexpr int S0 = U;              // slot of row j
@@ -219,6 +242,37 @@ __global__ __launch_bounds__(64) void getrf_lean64_kernel(WinParams P) {
                 }
             }
         }
+        if constexpr (FWD) {
+            // ---- forward solve, one step behind: the update of step j-1
+            // (its multipliers and y(j-1) are at hand, so these instructions
+            // wait for nothing on this step's chain), then the interchange of
+            // step j and y(j); step j's update waits for step j+1
+            if constexpr (H > 1) {
+#pragma unroll
+                for (int t = 1; t < H; ++t)
+                    bw[(S0 + t - 1) & 15] = __builtin_fma(-lp[t], yp, bw[(S0 + t - 1) & 15]);
+            }
+            const double b0 = bw[S0];
+            double bj = b0;
+            if constexpr (H > 1) {
+                double bp = bw[(S0 + 1) & 15];
+#pragma unroll
+                for (int k = 2; k < H; ++k) bp = p == k ? bw[(S0 + k) & 15] : bp;
+                bj = p != 0 ? bp : b0;
+#pragma unroll
+                for (int k = 1; k < H; ++k) bw[(S0 + k) & 15] = p == k ? b0 : bw[(S0 + k) & 15];
+#pragma unroll
+                for (int t = 1; t < H; ++t) lp[t] = own_copy(nz ? lm[t] : cv[t]);  // the column as stored
+            }
+            yp = own_copy(bj);
+            yv = L == U ? bj : yv;
+            // row j+H enters (step j's update, applied at step j+1, reaches
+            // rows j+1..j+kl only).  The b window, the last multipliers and y
+            // sit in vector registers (own_copy): as scalars they crowd out
+            // the step's scalar registers, which then spill to vector lanes.
+            bw[(S0 + H) & 15] =
+                own_copy(U + H < PF ? readlane_d(bcur, (U + H) & 15) : readlane_d(bnext, (U + H) & 15));
+        }
     };
 
     auto block = [&]<bool LEAN>(int j0) __attribute__((always_inline)) {
@@ -230,6 +284,11 @@ __global__ __launch_bounds__(64) void getrf_lean64_kernel(WinParams P) {
             }
         }(std::make_integer_sequence<int, PF>{});
         buf_st_i32(pb, (L < PF && j0 + L < n) ? uint32_t(j0 + L) * 4u : kOutside, pv);
+        if constexpr (FWD) {
+            buf_st(bb, (L < PF && j0 + L < n) ? uint32_t(j0 + L) * 8u : kOutside, yv);
+            bcur = own_copy(bnext);
+            bnext = buf_ld(bb, (L < PF && j0 + 2 * PF + L < n) ? uint32_t(j0 + 2 * PF + L) * 8u : kOutside);
+        }
     };
 
     // lean block: stores of columns >= 0 (j0 >= 16 > H - 1), loads of rows and

@@ -40,6 +40,10 @@ struct WinParams {
     int n, ku, batch;
     int kl;      // read by the kernels that take kl at run time
     int resume;  // two-wavefront and lean window kernels: continue where the diagonal-pivot kernel stopped
+    // lean window kernel with the forward solve: one right-hand side per
+    // matrix, B + b * strideB (set only for that kernel)
+    double *B = nullptr;
+    int64_t strideB = 0;
 };
 
 template <int G>

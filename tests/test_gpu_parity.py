@@ -265,6 +265,60 @@ def test_getrf_window_lean_special(kl, ku):
     check_exact(random_band(n, kl, ku, 99) * 1e-305, kl, ku, "tiny", variant="window")
 
 
+def gbsv_lean_case(T, kl, ku, seed):
+    """band_gbsv_lu + band_gbsv_back with one right-hand side (the lean
+    window kernel runs the forward solve in its own steps) against the
+    oracle's gbtrf + gbtrs, and against band_getrf + band_getrs."""
+    n = T.shape[0]
+    b = np.random.default_rng(seed).standard_normal((1, n))
+    A = to_dev(T)
+    AB1 = bandlu.dense_to_band(A, kl, ku)
+    AB2 = AB1.clone()
+    B1, B2 = to_dev(b), to_dev(b)
+    ip1, inf1 = bandlu.band_getrf(AB1, kl, ku)
+    bandlu.band_getrs(AB1, kl, ku, ip1, B1)
+    ip2, inf2 = bandlu.band_gbsv_lu(AB2, kl, ku, B2)
+    bandlu.band_gbsv_back(AB2, kl, ku, B2)
+    torch.cuda.synchronize()
+    ABo, _ = oracle.dense_to_band(T, kl, ku)
+    ipo, info_o, _ = oracle.gbtrf(ABo, kl, ku)
+    xo = b.copy()
+    oracle.gbtrs(ABo, kl, ku, ipo, xo)
+    what = f"gbsv n={n} kl={kl} ku={ku}"
+    assert np.array_equal(ip2.cpu().numpy(), ipo) and int(inf2.cpu()[0]) == info_o, what
+    assert_bitwise(AB2.cpu().numpy(), ABo, what + ": factors")
+    assert_bitwise(B2.cpu().numpy(), xo, what + ": solution")
+    assert torch.equal(ip1, ip2) and torch.equal(inf1, inf2)
+    assert_bitwise(B2.cpu().numpy(), B1.cpu().numpy(), what + ": fused vs two calls")
+
+
+@pytest.mark.parametrize("n,kl,ku", [(601, 1, 40), (555, 2, 64), (700, 3, 30), (640, 4, 40),
+                                     (603, 5, 100), (650, 6, 50), (700, 6, 115), (33, 2, 30),
+                                     (30, 1, 29), (40, 6, 30), (97, 3, 25)])
+def test_gbsv_lean_fused(n, kl, ku):
+    print(f"gbsv lean n={n} kl={kl} ku={ku}", flush=True)
+    assert bandlu.band_getrf_variant(n, kl, ku) == "window"
+    for shift in (0.0, float(kl + ku)):
+        T = random_band(n, kl, ku, 4242 + n + kl, shift=shift)
+        gbsv_lean_case(T, kl, ku, 17 + n)
+
+
+@pytest.mark.parametrize("kl,ku", [(2, 64), (5, 30)])
+def test_gbsv_lean_fused_special(kl, ku):
+    """A zero column (its multipliers stay unscaled and enter the forward
+    solve as stored), NaN and Inf entries and a subnormal pivot column."""
+    n = 640
+    T = random_band(n, kl, ku, 777 + kl)
+    T[:, 300] = 0.0
+    T[320, 320] = np.nan
+    T[400, 400 + min(ku, 1)] = np.inf
+    T[450 - min(ku, 2): 451 + kl, 450] *= 1e-310
+    gbsv_lean_case(T, kl, ku, 99)
+    T = random_band(n, kl, ku, 778 + kl)
+    T[450 - min(ku, 2): 451 + kl, 450] *= 1e-310
+    gbsv_lean_case(T, kl, ku, 98)
+
+
 # The diagonal-pivot kernel must give the oracle's factors bit for bit
 # whether every column keeps its diagonal pivot (dominant bands), a column
 # fails the check (the two-wavefront kernel takes over there) or the first

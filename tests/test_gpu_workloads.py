@@ -50,6 +50,15 @@ def test_single_workload(name):
     bandlu.band_getrs(AB, kl, ku, ipiv, xg)
     xo = oracle.gbtrs(ABo, kl, ku, ipo, b.copy())
     assert np.array_equal(bits(xg.cpu().numpy()), bits(xo))
+    # the two halves of band_gbsv, as the benchmark times them (for
+    # n16384_kl2_ku64 the forward solve runs inside the factorisation)
+    AB2 = torch.from_numpy(AB0).to(DEV)
+    x2 = torch.from_numpy(b.copy()).to(DEV)
+    ip2, inf2 = bandlu.band_gbsv_lu(AB2, kl, ku, x2)
+    bandlu.band_gbsv_back(AB2, kl, ku, x2)
+    assert np.array_equal(ip2.cpu().numpy(), ipo) and int(inf2.cpu()[0]) == 0
+    assert np.array_equal(bits(AB2.cpu().numpy()), bits(ABo))
+    assert np.array_equal(bits(x2.cpu().numpy()), bits(xo))
 
 
 def test_batched_workload():
