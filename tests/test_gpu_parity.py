@@ -319,6 +319,27 @@ def test_gbsv_lean_fused_special(kl, ku):
     gbsv_lean_case(T, kl, ku, 98)
 
 
+@pytest.mark.parametrize("seed", range(30))
+def test_lean_window_random(seed):
+    """Random shapes for the lean window kernel (kl <= 7, up to two columns
+    per lane), forced, with zeros, NaN and tiny entries planted at random,
+    and the fused forward solve where band_gbsv_lu takes it."""
+    rng = np.random.default_rng(5000 + seed)
+    kl = int(rng.integers(1, 8))
+    ku = int(rng.integers(0, 128 - 2 * kl))
+    n = int(rng.integers(max(kl, ku) + 1, 420))
+    T = random_band(n, kl, ku, 6000 + seed, shift=float(rng.choice([0.0, 0.0, kl + ku])))
+    for _ in range(int(rng.integers(0, 4))):
+        i = int(rng.integers(0, n))
+        j = int(rng.integers(max(0, i - kl), min(n, i + ku + 1)))
+        T[i, j] = rng.choice([0.0, -0.0, np.nan, 1e-310, np.inf])
+    if seed % 5 == 0:
+        T[:, int(rng.integers(0, n))] = 0.0
+    check_exact(T, kl, ku, f"lean random n={n} kl={kl} ku={ku}", variant="window")
+    if kl <= 6 and bandlu.band_getrf_variant(n, kl, ku) == "window":
+        gbsv_lean_case(T, kl, ku, 7000 + seed)
+
+
 # The diagonal-pivot kernel must give the oracle's factors bit for bit
 # whether every column keeps its diagonal pivot (dominant bands), a column
 # fails the check (the two-wavefront kernel takes over there) or the first
