@@ -58,6 +58,18 @@ __device__ __forceinline__ void buf_st_i32(Buf b, uint32_t byte_off, int v) {
     __builtin_amdgcn_raw_buffer_store_b32((unsigned)v, b.r, byte_off, 0, 0);
 }
 
+// A copy into a vector register of its own.  A value that moves from a
+// prefetch register into a window slot is otherwise renamed, not copied: the
+// ring's registers then rotate through the slots, and a loop's back edge
+// needs copies of registers whose loads are still in flight (a wait for the
+// newest load of the block).  It also keeps a wave-uniform value out of the
+// scalar registers.
+__device__ __forceinline__ double own_copy(double x) {
+    double y;
+    asm("v_mov_b64 %0, %1" : "=&v"(y) : "v"(x));
+    return y;
+}
+
 __device__ __forceinline__ double readlane_d(double v, int lane) {
     const long long x = __double_as_longlong(v);
     const int lo = __builtin_amdgcn_readlane((int)(x & 0xffffffffll), lane);

@@ -203,31 +203,42 @@ __global__ __launch_bounds__(64) void getrf_g16_kernel(WinParams P) {
         // retired ones); row j+H enters its slot from the prefetch ring
         if constexpr (LEAN) {
             buf_st_so(ab, st_tab[U], soff, a[S0]);
-            a[(S0 + H) & 15] = pf[U];
+            a[(S0 + H) & 15] = own_copy(pf[U]);
             pf[U] = buf_ld_so(ab, ld_tab[U], soff);
         } else {
             const int co = colof(j - H + 1);
             const bool ok = co < n && j >= co - kv;
             buf_st(ab, ok ? mbase + uint32_t(co * ldab + kv + j - co) * 8u : kOutside, a[S0]);
-            a[(S0 + H) & 15] = pf[U];
+            a[(S0 + H) & 15] = own_copy(pf[U]);
             pf[U] = buf_ld(ab, foff(j + PF + H, colof(j + PF + 1)));
         }
     };
 
-    for (int j0 = 0; j0 < n; j0 += PF) {
-        // lean block: stores of columns >= 0 (j0 >= 16 > H - 1), loads of
-        // rows and columns < n, and kl candidates at every step
-        const bool lean = j0 >= PF && j0 + 2 * PF + kv + H < n;
-        if (lean) {
-            [&]<int... Us>(std::integer_sequence<int, Us...>) {
+    auto block = [&]<bool LEAN>(int j0) __attribute__((always_inline)) {
+        [&]<int... Us>(std::integer_sequence<int, Us...>) __attribute__((always_inline)) {
+            if constexpr (LEAN) {
                 (step.template operator()<Us, true>(j0 + Us, uint32_t(j0 + Us - PF) * uint32_t(ldab) * 8u), ...);
-            }(std::make_integer_sequence<int, PF>{});
-        } else {
-            [&]<int... Us>(std::integer_sequence<int, Us...>) {
+            } else {
                 ((j0 + Us < n ? step.template operator()<Us, false>(j0 + Us, 0u) : (void)0), ...);
-            }(std::make_integer_sequence<int, PF>{});
-        }
+            }
+        }(std::make_integer_sequence<int, PF>{});
         buf_st_i32(pb, j0 + gl < n ? pbase + uint32_t(j0 + gl) * 4u : kOutside, pv);
+    };
+    // lean block: stores of columns >= 0 (j0 >= 16 > H - 1), loads of rows
+    // and columns < n, and kl candidates at every step.  The lean blocks run
+    // in a loop of their own (no join with the other block's code at the
+    // loop head, where every load in flight would be waited for).
+    auto lean = [&](int j0) { return j0 >= PF && j0 + 2 * PF + kv + H < n; };
+    for (int j0 = 0; j0 < n;) {
+        if (lean(j0)) {
+            do {
+                block.template operator()<true>(j0);
+                j0 += PF;
+            } while (lean(j0));
+        } else {
+            block.template operator()<false>(j0);
+            j0 += PF;
+        }
     }
     if (live && gl == 0) P.info[b] = info;
 }

@@ -46,17 +46,6 @@
 
 namespace bandlu {
 
-// A copy into a register of its own.  A row entering the window moves from
-// its prefetch register into a window slot; left to itself the register
-// allocator renames instead of copying, so the ring's registers rotate
-// through the slots and the loop's back edge needs copies of registers whose
-// loads are still in flight (a wait for the newest load of the block).
-__device__ __forceinline__ double own_copy(double x) {
-    double y;
-    asm("v_mov_b64 %0, %1" : "=&v"(y) : "v"(x));
-    return y;
-}
-
 template <int H, int CPL, bool FWD = false>
 __global__ __launch_bounds__(64) void getrf_lean64_kernel(WinParams P) {
     static_assert(H >= 1 && H <= 8, "kl <= 7");

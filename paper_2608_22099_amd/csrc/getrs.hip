@@ -400,23 +400,32 @@ __global__ __launch_bounds__(64) void getrs_g16_kernel(RsParams P, int64_t syste
             else
                 lr[u] = buf_ld(ab, loff(u, j + 16));
         };
-        for (int j0 = 0; j0 < n - 1; j0 += 16) {
+        auto fblock = [&]<bool LEAN>(int j0) __attribute__((always_inline)) {
             const int ipv_next =
                 buf_ld_i32(pb, j0 + 16 + gl < n ? pbase + uint32_t(j0 + 16 + gl) * 4u : kOutside);
             const double nxt_next = buf_ld(xb, rowoff(j0 + 32 + gl));
             double done = 0.0;
-            if (j0 + 32 + KL <= n) {
-                [&]<int... Us>(std::integer_sequence<int, Us...>) {
-                    (fstep.template operator()<Us, true>(j0, done), ...);
-                }(std::make_integer_sequence<int, 16>{});
-            } else {
-                [&]<int... Us>(std::integer_sequence<int, Us...>) {
-                    (fstep.template operator()<Us, false>(j0, done), ...);
-                }(std::make_integer_sequence<int, 16>{});
-            }
+            [&]<int... Us>(std::integer_sequence<int, Us...>) __attribute__((always_inline)) {
+                (fstep.template operator()<Us, LEAN>(j0, done), ...);
+            }(std::make_integer_sequence<int, 16>{});
             buf_st(xb, j0 + gl < n - 1 ? rowoff(j0 + gl) : kOutside, done);
             ipv = ipv_next;
             nxt = nxt_next;
+        };
+        // the lean blocks run in a loop of their own (no join with the other
+        // block's code at the loop head, where every load in flight would be
+        // waited for)
+        auto flean = [&](int j0) { return j0 + 32 + KL <= n; };
+        for (int j0 = 0; j0 < n - 1;) {
+            if (flean(j0)) {
+                do {
+                    fblock.template operator()<true>(j0);
+                    j0 += 16;
+                } while (flean(j0));
+            } else {
+                fblock.template operator()<false>(j0);
+                j0 += 16;
+            }
         }
         buf_st(xb, gl == ((n - 1) & 15) ? rowoff(n - 1) : kOutside, bv);
         __threadfence();
@@ -457,20 +466,27 @@ __global__ __launch_bounds__(64) void getrs_g16_kernel(RsParams P, int64_t syste
             else
                 ur[u] = buf_ld(ab, uoff(u, j - 16));
         };
-        for (int m0 = 0; m0 < n; m0 += 16) {
+        auto bblock = [&]<bool LEAN>(int m0) __attribute__((always_inline)) {
             const double nxt = buf_ld(xb, rowoff(n - 1 - (m0 + 16 + gl)));
             double done = 0.0;
-            // lean: every step of the block has j >= max(32, kv)
-            if (m0 + 48 + kv <= n) {
-                [&]<int... Us>(std::integer_sequence<int, Us...>) {
-                    (bstep.template operator()<Us, true>(m0, done, nxt), ...);
-                }(std::make_integer_sequence<int, 16>{});
-            } else {
-                [&]<int... Us>(std::integer_sequence<int, Us...>) {
-                    (bstep.template operator()<Us, false>(m0, done, nxt), ...);
-                }(std::make_integer_sequence<int, 16>{});
-            }
+            [&]<int... Us>(std::integer_sequence<int, Us...>) __attribute__((always_inline)) {
+                (bstep.template operator()<Us, LEAN>(m0, done, nxt), ...);
+            }(std::make_integer_sequence<int, 16>{});
             buf_st(xb, rowoff(n - 1 - (m0 + gl)), done);
+        };
+        // lean: every step of the block has j >= max(32, kv); the lean blocks
+        // run in a loop of their own, as in the forward pass
+        auto blean = [&](int m0) { return m0 + 48 + kv <= n; };
+        for (int m0 = 0; m0 < n;) {
+            if (blean(m0)) {
+                do {
+                    bblock.template operator()<true>(m0);
+                    m0 += 16;
+                } while (blean(m0));
+            } else {
+                bblock.template operator()<false>(m0);
+                m0 += 16;
+            }
         }
     }
 }
