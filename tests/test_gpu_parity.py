@@ -544,8 +544,11 @@ def test_getrf_fill_rows_not_read():
 
 
 @pytest.mark.parametrize("kl,ku,batch,n", [(4, 4, 256, 64), (1, 2, 100, 33), (7, 3, 70, 50),
-                                           (4, 4, 3, 64), (10, 5, 65, 40), (3, 20, 64, 90)])
+                                           (4, 4, 3, 64), (10, 5, 65, 40), (3, 20, 64, 90),
+                                           (3, 30, 5, 300), (2, 64, 7, 200), (6, 40, 63, 120)])
 def test_getrf_batched(kl, ku, batch, n):
+    # (the last three: batches below 64 beyond the sixteen-lane and diagonal
+    # kernels, which the lean window kernel factors one matrix per workgroup)
     T = np.stack([random_band(n, kl, ku, 500 + b) for b in range(batch)])
     T[1 % batch, 3, :] = 0.0  # one singular matrix
     A = to_dev(T)
