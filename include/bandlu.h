@@ -215,13 +215,15 @@ int band_getrs_batched(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const do
  * BANDLU_GETRF_* codes below, or a negative status for invalid sizes.
  */
 #define BANDLU_GETRF_WINDOW 1       /* register window, 64 lanes per matrix     */
+                                    /* (kl <= 7: the pivot decided on scalars)  */
 #define BANDLU_GETRF_WINDOW_G16 2   /* register window, 16 lanes per matrix     */
 #define BANDLU_GETRF_GENERIC 3      /* unblocked, one workgroup per matrix      */
 #define BANDLU_GETRF_BLOCKED 4      /* blocked, exact rank-1 trailing updates   */
 #define BANDLU_GETRF_BLOCKED_MFMA 5 /* blocked, fp64 MFMA trailing update       */
 #define BANDLU_GETRF_SPLIT 6        /* register window + a pivot wavefront      */
-#define BANDLU_GETRF_DIAG 7         /* diagonal pivots verified per column, the */
-                                    /* split kernel from the first failing one  */
+#define BANDLU_GETRF_DIAG 7         /* diagonal pivots verified per column; the */
+                                    /* window (kl <= 6) or split kernel from    */
+                                    /* the first failing one                    */
 #define BANDLU_GETRF_WIDE 8         /* one persistent launch: blocks of 32      */
                                     /* columns in LDS, matrix-core updates      */
 int band_getrf_variant(int64_t n, int64_t kl, int64_t ku, int64_t batch);
@@ -277,8 +279,10 @@ int band_getrs_ex(int64_t n, int64_t kl, int64_t ku, int64_t nrhs, const double 
  *     B <- L^-1 P B.  When the persistent wide-band LU factors the matrix (see
  *     band_getrf) and nrhs <= 33, the forward half runs inside that launch:
  *     one more workgroup trails the chain of panels and applies each
- *     published panel to the right-hand sides.  Otherwise the forward chain
- *     runs after the factorisation.
+ *     published panel to the right-hand sides.  When nrhs = 1 and the
+ *     64-lane window kernel with scalar pivots factors it (1 <= kl <= 6, see
+ *     band_getrf_variant), the forward half runs inside that kernel's column
+ *     steps.  Otherwise the forward chain runs after the factorisation.
  *   - band_gbsv_back: the backward half, B <- U^-1 B, from the factors.
  * As in band_getrs, B is solved even when *d_info > 0 (a zero pivot then
  * gives IEEE infinities or NaN; LAPACK's xGBSV would skip the solve).
