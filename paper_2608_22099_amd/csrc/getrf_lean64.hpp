@@ -217,8 +217,10 @@ __global__ __launch_bounds__(64) void getrf_lean64_kernel(WinParams P) {
             // redone from the kept entries.  Placed last, this one rare branch
             // leaves the rest of the step in one scheduling region.
             if (__builtin_expect(!(fabs(best) >= DBL_MIN), 0)) {
+                // (a zero pivot leaves its column as it is: the forward solve
+                // then reads the multipliers as stored, the raw column)
 #pragma unroll
-                for (int t = 1; t < H; ++t) lm[t] = cs[t] / best;
+                for (int t = 1; t < H; ++t) lm[t] = nz ? cs[t] / best : cv[t];
 #pragma unroll
                 for (int t = 1; t < H; ++t) a[SJ][(S0 + t) & 15] = own ? lm[t] : a[SJ][(S0 + t) & 15];
 #pragma unroll
@@ -251,7 +253,7 @@ __global__ __launch_bounds__(64) void getrf_lean64_kernel(WinParams P) {
 #pragma unroll
                 for (int k = 1; k < H; ++k) bw[(S0 + k) & 15] = p == k ? b0 : bw[(S0 + k) & 15];
 #pragma unroll
-                for (int t = 1; t < H; ++t) lp[t] = own_copy(nz ? lm[t] : cv[t]);  // the column as stored
+                for (int t = 1; t < H; ++t) lp[t] = own_copy(lm[t]);  // the column as stored
             }
             yp = own_copy(bj);
             yv = L == U ? bj : yv;
