@@ -508,7 +508,9 @@ def band_gbsv(AB, kl, ku, B, ipiv=None, info=None):
 
 def band_gbsv_lu(AB, kl, ku, B, ipiv=None, info=None):
     """The first half of band_gbsv: band_getrf, and B <- L^-1 P B (inside the
-    persistent wide-band launch where it runs).  Returns (ipiv, info)."""
+    persistent wide-band launch where it runs, and inside the 64-lane window
+    kernel's steps for one right-hand side with 1 <= kl <= 6).  Returns
+    (ipiv, info)."""
     _check(AB, torch.float64, "AB", 2)
     _check(B, torch.float64, "B", 2)
     n = AB.shape[0]
